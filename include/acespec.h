@@ -1,0 +1,177 @@
+/*
+ * acespec.h -- C ABI of the MI355X (gfx950) tree-verification library.
+ *
+ * The library implements the cloud side of AceSpec's edge-cloud speculative decoding
+ * (Section III-B, "Verify Loop"): one forward pass of a decoder-only target model over a
+ * batch of drafted token trees, each node attending to its session's KV prefix and to its
+ * own ancestors (Section III-C, tree attention mask), followed by the per-node reduction
+ * of the target distribution to what the downlink carries (Algorithm 1, RECEIVE_WAIT
+ * returns the rejection index and a sparse target distribution): the min(1, p/q)
+ * acceptance test against the draft distribution, the residual max(0, p - q) resample,
+ * a bonus sample, and a top-k sparse distribution; then the per-session path walk with
+ * the sibling-hit rule of Algorithm 1 (the resampled token looked up among the drafted
+ * alternatives).
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers, owned by the caller; the library never
+ *    frees them.  Layouts are dense row-major with the shapes given in the comments.
+ *  - Work is enqueued on `stream`; the call returns without synchronising and the
+ *    outputs are valid once the stream has completed.
+ *  - Argument and shape errors are reported synchronously, before anything is
+ *    launched, by a negative return code; acespec_last_error() then holds a message.
+ *  - Malformed per-session data found on the device (a parent index that is not an
+ *    earlier row, a token id outside the vocabulary, a prefix length that does not fit
+ *    the cache) sets status[b] = ACESPEC_EBADTREE for that session only; its other
+ *    outputs are then unspecified but every access stays in bounds.
+ *  - No C++ exception crosses this interface.
+ *  - A context must not be used by two calls that overlap in time (its workspace is
+ *    shared by all calls on it).
+ */
+#ifndef ACESPEC_H
+#define ACESPEC_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ACESPEC_OK = 0,
+  ACESPEC_EINVAL = -1,        /* bad argument (null pointer, size out of range, ...)   */
+  ACESPEC_EUNSUPPORTED = -2,  /* valid but not supported by these kernels            */
+  ACESPEC_ENOMEM = -3,        /* workspace allocation failed in acespec_create        */
+  ACESPEC_EHIP = -4,          /* a HIP runtime call failed                            */
+  ACESPEC_EBADTREE = -5       /* per-session status only: malformed tree or prefix    */
+} acespec_status;
+
+typedef enum { ACESPEC_F32 = 0, ACESPEC_BF16 = 1 } acespec_dtype;
+
+/* Decoder shape.  The paper names only the model families (Qwen, LLaMA; Section V-A);
+ * the reading implemented is a Llama-style pre-norm decoder: RMSNorm with gains,
+ * rotate-half RoPE (theta_i = rope_base^(-2i/head_dim)), grouped-query attention with
+ * scale 1/sqrt(head_dim), SwiGLU MLP, no biases, untied LM head.
+ * Supported: head_dim in {64, 128}; n_heads % n_kv_heads == 0;
+ * d_model, n_heads*head_dim and d_ff multiples of 64; vocab a multiple of 4. */
+typedef struct {
+  int n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rope_base;   /* e.g. 10000 */
+  float rms_eps;     /* e.g. 1e-5  */
+  acespec_dtype dtype;  /* weights, activations between kernels and KV cache */
+} acespec_model_desc;
+
+/* Per-layer weights, all in the model dtype, row-major [out, in] (K contiguous). */
+typedef struct {
+  const void *attn_norm;   /* [d_model]                                              */
+  const void *wqkv;        /* [(n_heads + 2 n_kv_heads) head_dim, d_model]: q, k, v rows */
+  const void *wo;          /* [d_model, n_heads head_dim]                             */
+  const void *mlp_norm;    /* [d_model]                                               */
+  const void *w_gate_up;   /* [2 d_ff, d_model]: gate rows then up rows                */
+  const void *w_down;      /* [d_model, d_ff]                                         */
+} acespec_layer_weights;
+
+typedef struct {
+  const void *embed;                     /* [vocab, d_model]                           */
+  const acespec_layer_weights *layers;   /* HOST array of n_layers entries              */
+  const void *final_norm;                /* [d_model]                                  */
+  const void *lm_head;                   /* [vocab, d_model]                           */
+} acespec_weights;
+
+/* KV cache, in the model dtype: k and v are each [n_layers][B][n_kv_heads][capacity]
+ * [head_dim], keys stored after RoPE.  Slots [0, prefix_len[b]) hold session b's
+ * verified context and are only read.  The verify call writes the tree's keys and
+ * values into slots prefix_len[b] + r for tree rows r = 0..N (nothing is committed:
+ * calling again with the same inputs gives the same result). */
+typedef struct {
+  void *k, *v;
+  int capacity;                 /* slots per (layer, session, kv head)                  */
+  const int32_t *prefix_len;    /* [B] DEVICE; needs prefix_len[b] + N + 1 <= capacity */
+} acespec_kv_cache;
+
+/* Target sampling parameters (Section III-B: nucleus sampling on the target side). */
+typedef struct {
+  float temperature;   /* > 0: logits are divided by it                               */
+  float top_p;         /* (0, 1]: smallest most-probable set reaching this mass        */
+  int top_k;           /* 1..256 and <= vocab: size of the sparse downlink payload     */
+} acespec_params;
+
+/* Caller-allocated device outputs.  Row counts: B*(N+1) rows for verify_tree (row 0 of
+ * each session is the root), R rows for verify_tail. */
+typedef struct {
+  uint8_t *accept;          /* [rows] 1 if the row's token is accepted by its parent's
+                               distribution (root rows: 1)                             */
+  int32_t *acc_prefix_len;  /* [rows] leading accepted nodes on the root-to-row path  */
+  int32_t *resample_token;  /* [rows] residual inverse-CDF sample (root rows: -1)     */
+  int32_t *bonus_token;     /* [rows] sample from the row's own target distribution   */
+  int32_t *topk_ids;        /* [rows, top_k] most probable first                      */
+  float   *topk_probs;      /* [rows, top_k] renormalised over the k ids (0 outside
+                               the top-p nucleus)                                     */
+  int32_t *path;            /* [B, N+1] kept drafted rows root-first, -1 padded       */
+  int32_t *path_len;        /* [B] drafted tokens kept                                */
+  int32_t *next_token;      /* [B] token emitted after the kept path                  */
+  uint8_t *sibling_hit;     /* [B] 1 if the walk continued through a drafted sibling */
+  int32_t *status;          /* [B] ACESPEC_OK or ACESPEC_EBADTREE                     */
+  float   *logits_out;      /* optional [rows, vocab] fp32 logits; NULL = not kept    */
+} acespec_outputs;
+
+typedef struct acespec_ctx acespec_ctx;
+
+/* Creates a context on the current HIP device and allocates its workspace for up to
+ * max_batch sessions of up to max_nodes drafted nodes (max_nodes <= 64), i.e.
+ * max_batch*(max_nodes+1) rows.  The same bound limits verify_tail's row count.
+ * Returns ACESPEC_OK and *out, or an error (ENOMEM if the workspace does not fit). */
+int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
+                   acespec_ctx **out);
+
+/* Frees the workspace (synchronises the device first).  NULL is accepted. */
+void acespec_destroy(acespec_ctx *ctx);
+
+/* One verify step over B drafted trees of N drafted nodes each.
+ *  tree_tokens [B, N+1] int32: row 0 is the root (the last committed token, not yet in
+ *                the cache), rows 1..N the drafted tokens.
+ *  parent_idx  [B, N+1] int32: parent_idx[b,0] = -1 and 0 <= parent_idx[b,r] < r.
+ *                The lowest-index child of a row is its main-chain child.
+ *  draft_q     [B, N+1, vocab] fp32: row r holds the draft distribution that proposed
+ *                r's children; only rows with children are read.
+ *  uniforms    [B, N+1, 3] fp32 in (0, 1): per row (accept, residual, bonus).
+ * Writes every field of *outs (logits_out only if non-NULL). */
+int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *weights,
+                        const acespec_kv_cache *kv, const int32_t *tree_tokens,
+                        const int32_t *parent_idx, const float *draft_q,
+                        const float *uniforms, int B, int N, const acespec_params *params,
+                        const acespec_outputs *outs, hipStream_t stream);
+
+/* LM head and verification only, over R given hidden states (the last stage of
+ * verify_tree on its own).  Each row r is the parent of one drafted token
+ * draft_tokens[r]; rows form chains of chain_len consecutive rows (R % chain_len == 0).
+ *  lm_head [vocab, d_model], final_norm [d_model] or NULL (no normalisation),
+ *  hidden [R, d_model] in the model dtype, draft_q [R, vocab], uniforms [R, 3].
+ * Per row: accept, resample_token, bonus_token, topk_*, acc_prefix_len (leading accepts
+ * within its chain, counting the row).  Per chain c: path_len[c] = leading accepts,
+ * path[c, 0..chain_len) = kept row indices within the chain (-1 padded),
+ * next_token[c] = resample at the first rejected row, or -1 when the whole chain is
+ * accepted (the bonus then needs the row after the chain); sibling_hit[c] = 0,
+ * status[c] = OK.  path is [R/chain_len, chain_len]. */
+int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
+                        const void *hidden, const int32_t *draft_tokens,
+                        const float *draft_q, const float *uniforms, int R, int chain_len,
+                        const acespec_params *params, const acespec_outputs *outs,
+                        hipStream_t stream);
+
+/* Message for the last non-OK return on this thread ("" if none). */
+const char *acespec_last_error(void);
+
+/* Per-kernel timing with HIP events recorded on the launch stream around every
+ * kernel.  enable != 0 turns it on for subsequent calls.  acespec_timing_read waits
+ * for the recorded events, returns per-kernel-kind totals accumulated since the last
+ * read (names[i], total_ms[i], launches[i] for i < returned count, at most max
+ * entries) and clears them.  names point to static strings. */
+int acespec_timing_enable(acespec_ctx *ctx, int enable);
+int acespec_timing_read(acespec_ctx *ctx, const char **names, double *total_ms,
+                        int *launches, int max);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ACESPEC_H */

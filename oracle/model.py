@@ -142,46 +142,54 @@ def validate_tree(parents: Sequence[int], tokens: Sequence[int], V: int) -> bool
 # ----------------------------------------------------------------------------------------
 
 
+def tree_layer(W: F64Weights, dims: Dims, l: int, x: np.ndarray, kpre: np.ndarray,
+               vpre: np.ndarray, cos: np.ndarray, sin: np.ndarray, anc: np.ndarray,
+               S: int) -> np.ndarray:
+    """One decoder layer over the n rows of one tree.  kpre / vpre: [Hkv, S, hd] prefix
+    (keys post-RoPE).  Row r attends to the S prefix slots and to rows j with anc[r, j]."""
+    n = x.shape[0]
+    H, Hkv, hd, G = dims.H, dims.Hkv, dims.hd, dims.G
+    scale = 1.0 / np.sqrt(hd)
+    a = rms_norm(x, W.get("attn_norm", l), dims.rms_eps)
+    qkv = a @ W.get("wqkv", l).T
+    q = qkv[:, : H * hd].reshape(n, H, hd)
+    k = qkv[:, H * hd: (H + Hkv) * hd].reshape(n, Hkv, hd)
+    v = qkv[:, (H + Hkv) * hd:].reshape(n, Hkv, hd)
+    q = apply_rope(q, cos, sin)
+    k = apply_rope(k, cos, sin)
+    o = np.zeros((n, H, hd))
+    visible = np.concatenate([np.ones((n, S), dtype=bool), anc], axis=1)
+    for h in range(H):
+        g = h // G
+        keys = np.concatenate([kpre[g], k[:, g, :]], axis=0)      # [S + n, hd]
+        vals = np.concatenate([vpre[g], v[:, g, :]], axis=0)
+        s = (q[:, h, :] @ keys.T) * scale                          # [n, S + n]
+        s = np.where(visible, s, -np.inf)
+        o[:, h, :] = softmax_rows(s) @ vals
+    x = x + o.reshape(n, H * hd) @ W.get("wo", l).T
+    b = rms_norm(x, W.get("mlp_norm", l), dims.rms_eps)
+    gu = b @ W.get("w_gate_up", l).T
+    return x + (silu(gu[:, : dims.F]) * gu[:, dims.F:]) @ W.get("w_down", l).T
+
+
+def final_logits(W: F64Weights, dims: Dims, x: np.ndarray) -> np.ndarray:
+    return rms_norm(x, W.get("final_norm"), dims.rms_eps) @ W.get("lm_head").T
+
+
 def forward_tree_session(W: F64Weights, dims: Dims, kpre: List[np.ndarray],
                          vpre: List[np.ndarray], tokens: Sequence[int],
-                         parents: Sequence[int], S: int, final: bool = True) -> np.ndarray:
+                         parents: Sequence[int], S: int) -> np.ndarray:
     """Logits z[r] (float64, [n, V]) for every row of one drafted tree.
 
     kpre / vpre: per layer, the session's cache prefix [Hkv, S, hd] (keys post-RoPE).
-    Row r attends to the S prefix slots and to the rows j with anc[r, j].
     """
-    n = len(tokens)
-    H, Hkv, hd, G = dims.H, dims.Hkv, dims.hd, dims.G
     depth = np.array(tree_depths(parents))
-    pos = S + depth
     anc = ancestor_matrix(parents)
-    cos, sin = rope_cos_sin(pos, hd, dims.rope_base)
+    cos, sin = rope_cos_sin(S + depth, dims.hd, dims.rope_base)
     x = W.embed_rows(tokens)
-    scale = 1.0 / np.sqrt(hd)
     for l in range(dims.L):
-        a = rms_norm(x, W.get("attn_norm", l), dims.rms_eps)
-        qkv = a @ W.get("wqkv", l).T
-        q = qkv[:, : H * hd].reshape(n, H, hd)
-        k = qkv[:, H * hd: (H + Hkv) * hd].reshape(n, Hkv, hd)
-        v = qkv[:, (H + Hkv) * hd:].reshape(n, Hkv, hd)
-        q = apply_rope(q, cos, sin)
-        k = apply_rope(k, cos, sin)
-        o = np.zeros((n, H, hd))
-        for h in range(H):
-            g = h // G
-            keys = np.concatenate([kpre[l][g], k[:, g, :]], axis=0)      # [S + n, hd]
-            vals = np.concatenate([vpre[l][g], v[:, g, :]], axis=0)
-            s = (q[:, h, :] @ keys.T) * scale                              # [n, S + n]
-            visible = np.concatenate([np.ones((n, S), dtype=bool), anc], axis=1)
-            s = np.where(visible, s, -np.inf)
-            o[:, h, :] = softmax_rows(s) @ vals
-        x = x + o.reshape(n, H * hd) @ W.get("wo", l).T
-        b = rms_norm(x, W.get("mlp_norm", l), dims.rms_eps)
-        gu = b @ W.get("w_gate_up", l).T
-        x = x + (silu(gu[:, : dims.F]) * gu[:, dims.F:]) @ W.get("w_down", l).T
-    if not final:
-        return x
-    return rms_norm(x, W.get("final_norm"), dims.rms_eps) @ W.get("lm_head").T
+        x = tree_layer(W, dims, l, x, kpre[l], vpre[l], cos, sin, anc, S)
+    return final_logits(W, dims, x)
 
 
 # ----------------------------------------------------------------------------------------
@@ -253,22 +261,35 @@ def session_prefix(kv_k, kv_v, b: int, S: int):
             [to_f64(kv_v[l, b, :, :S]) for l in range(L)])
 
 
-def forward_tree_batch(weights, dims: Dims, batch, sessions: Sequence[int] = None,
-                       progress: Callable[[str], None] = None) -> np.ndarray:
-    """Logits [len(sessions), N+1, V] for the chosen sessions of a synthetic batch."""
+def forward_tree_batch(weights, dims: Dims, tokens, parents, prefix_len, kv_prefix,
+                       sessions: Sequence[int], progress: Callable[[str], None] = None,
+                       drop_layers: bool = True) -> np.ndarray:
+    """Logits [len(sessions), N+1, V] for the chosen sessions.
+
+    kv_prefix(l, b) -> (K [Hkv, S_b, hd], V [Hkv, S_b, hd]) gives session b's cache prefix
+    at layer l.  Layers run outermost so each layer's weights are converted once for all
+    sessions and can be dropped afterwards (the 8B shapes do not fit in fp64 at once).
+    """
     W = weights if isinstance(weights, F64Weights) else F64Weights(weights)
-    B = batch.tokens.shape[0]
-    sessions = list(range(B)) if sessions is None else list(sessions)
-    out = []
+    st = []
     for b in sessions:
-        S = int(batch.prefix_len[b])
-        kp, vp = session_prefix(batch.kv_k, batch.kv_v, b, S)
-        toks = [int(t) for t in batch.tokens[b]]
-        pars = [int(p) for p in batch.parents[b]]
-        out.append(forward_tree_session(W, dims, kp, vp, toks, pars, S))
+        S = int(prefix_len[b])
+        toks = [int(t) for t in tokens[b]]
+        pars = [int(p) for p in parents[b]]
+        depth = np.array(tree_depths(pars))
+        cos, sin = rope_cos_sin(S + depth, dims.hd, dims.rope_base)
+        st.append(dict(b=b, S=S, anc=ancestor_matrix(pars), cos=cos, sin=sin,
+                       x=W.embed_rows(toks)))
+    for l in range(dims.L):
+        for s in st:
+            kp, vp = kv_prefix(l, s["b"])
+            s["x"] = tree_layer(W, dims, l, s["x"], kp, vp, s["cos"], s["sin"], s["anc"],
+                                s["S"])
+        if drop_layers:
+            W.drop_layer(l)
         if progress:
-            progress(f"oracle forward session {b} done")
-    return np.stack(out)
+            progress(f"oracle layer {l + 1}/{dims.L} done")
+    return np.stack([final_logits(W, dims, s["x"]) for s in st])
 
 
 def lm_head_tail(weights, hidden, final_norm: bool = False, eps: float = 1e-5) -> np.ndarray:

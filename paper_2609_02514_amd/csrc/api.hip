@@ -1,0 +1,444 @@
+// Host side of the verify library: context and workspace, argument validation, the
+// launch sequence of one verify step, per-kernel event timing and error reporting.
+//
+// One verify step (Section III-B: the cloud runs one forward pass over the received
+// tokens, then checks them): tree prep -> embedding -> for each layer {RMSNorm, QKV
+// GEMM, RoPE + tree K/V write, tree attention, O GEMM + residual, RMSNorm, gate/up GEMM
+// + SwiGLU, down GEMM + residual} -> final RMSNorm -> LM head GEMM (fp32 logits) ->
+// fused vocabulary verify -> path walk.  Everything is enqueued on the caller's stream
+// without synchronisation and without allocation.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace acespec;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+enum Kind {
+  K_TREE, K_EMBED, K_RMSNORM, K_GEMM_QKV, K_ROPE, K_ATTN, K_GEMM_O, K_GEMM_GATE_UP,
+  K_GEMM_DOWN, K_GEMM_LM, K_VOCAB, K_WALK, K_COUNT
+};
+const char *kKindNames[K_COUNT] = {"tree_prep",    "embed",       "rmsnorm",
+                                   "gemm_qkv",     "rope_kv",     "tree_attention",
+                                   "gemm_o",       "gemm_gate_up", "gemm_down",
+                                   "gemm_lm_head", "vocab_verify", "path_walk"};
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+struct acespec_ctx {
+  acespec_model_desc d;
+  int max_batch = 0, max_nodes = 0, max_rows = 0;
+  size_t esz = 0;  // bytes per model-dtype element
+  void *ws = nullptr;
+  float *x = nullptr, *logits = nullptr, *part_o = nullptr, *part_ml = nullptr;
+  void *a = nullptr, *attn = nullptr, *qkv = nullptr, *h = nullptr;
+  long long part_cap = 0;
+  double *inv_freq = nullptr;
+  TreeMeta meta{};
+  // timing
+  bool timing = false;
+  struct Rec { int kind; hipEvent_t e0, e1; };
+  std::vector<hipEvent_t> free_events;
+  std::vector<Rec> pending;
+  double tot_ms[K_COUNT] = {};
+  int launches[K_COUNT] = {};
+};
+
+namespace {
+
+hipEvent_t get_event(acespec_ctx *c) {
+  if (!c->free_events.empty()) {
+    hipEvent_t e = c->free_events.back();
+    c->free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Runs one launch, bracketed by timing events when enabled.
+template <typename F>
+int run(acespec_ctx *c, int kind, hipStream_t s, F &&launch) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (c->timing) {
+    e0 = get_event(c);
+    e1 = get_event(c);
+    if (!e0 || !e1) return fail(ACESPEC_EHIP, "hipEventCreate failed");
+    if (hipEventRecord(e0, s) != hipSuccess) return fail(ACESPEC_EHIP, "hipEventRecord failed");
+  }
+  hipError_t err = launch();
+  if (err != hipSuccess)
+    return fail(ACESPEC_EHIP, "%s launch failed: %s", kKindNames[kind], hipGetErrorString(err));
+  if (c->timing) {
+    if (hipEventRecord(e1, s) != hipSuccess) return fail(ACESPEC_EHIP, "hipEventRecord failed");
+    c->pending.push_back({kind, e0, e1});
+  }
+  return ACESPEC_OK;
+}
+
+#define RUN(kind, expr)                                              \
+  do {                                                               \
+    int rc_ = run(ctx, kind, stream, [&]() -> hipError_t { return expr; }); \
+    if (rc_ != ACESPEC_OK) return rc_;                               \
+  } while (0)
+
+int check_params(const acespec_params *p, int V) {
+  if (!p) return fail(ACESPEC_EINVAL, "params is NULL");
+  if (!(p->temperature > 0.f) || !std::isfinite(p->temperature))
+    return fail(ACESPEC_EINVAL, "temperature must be finite and > 0 (got %g)", p->temperature);
+  if (!(p->top_p > 0.f && p->top_p <= 1.f))
+    return fail(ACESPEC_EINVAL, "top_p must be in (0, 1] (got %g)", p->top_p);
+  if (p->top_k < 1 || p->top_k > 256 || p->top_k > V)
+    return fail(ACESPEC_EINVAL, "top_k must be in [1, min(256, vocab)] (got %d)", p->top_k);
+  return ACESPEC_OK;
+}
+
+int check_outputs(const acespec_outputs *o) {
+  if (!o) return fail(ACESPEC_EINVAL, "outputs is NULL");
+  if (!o->accept || !o->acc_prefix_len || !o->resample_token || !o->bonus_token ||
+      !o->topk_ids || !o->topk_probs || !o->path || !o->path_len || !o->next_token ||
+      !o->sibling_hit || !o->status)
+    return fail(ACESPEC_EINVAL, "an output pointer is NULL (only logits_out may be)");
+  return ACESPEC_OK;
+}
+
+template <typename T>
+int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
+                     const int32_t *tokens, const int32_t *parents, const float *draft_q,
+                     const float *uniforms, int B, int N, const acespec_params *p,
+                     const acespec_outputs *o, hipStream_t stream) {
+  const acespec_model_desc &d = ctx->d;
+  const int n1 = N + 1, R = B * n1;
+  const int L = d.n_layers, D = d.d_model, H = d.n_heads, Hkv = d.n_kv_heads, hd = d.head_dim;
+  const int F = d.d_ff, V = d.vocab, QKVN = (H + 2 * Hkv) * hd;
+  const int cap = kv->capacity;
+  T *x_a = (T *)ctx->a, *x_attn = (T *)ctx->attn, *x_qkv = (T *)ctx->qkv, *x_h = (T *)ctx->h;
+  float *logits = o->logits_out ? o->logits_out : ctx->logits;
+  const TreeMeta &meta = ctx->meta;
+
+  RUN(K_TREE, launch_tree_prep(tokens, parents, kv->prefix_len, B, n1, V, cap, meta, o->status,
+                               stream));
+  RUN(K_EMBED, launch_embed<T>((const T *)w->embed, meta.tok, ctx->x, R, D, stream));
+  const size_t layer_stride = (size_t)B * Hkv * cap * hd;
+  for (int l = 0; l < L; ++l) {
+    const acespec_layer_weights &lw = w->layers[l];
+    T *ck = (T *)kv->k + l * layer_stride;
+    T *cv = (T *)kv->v + l * layer_stride;
+    RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)lw.attn_norm, x_a, R, D, d.rms_eps,
+                                     stream));
+    RUN(K_GEMM_QKV, launch_gemm<T>(EPI_STORE, x_a, (const T *)lw.wqkv, R, QKVN, D, x_qkv,
+                                   nullptr, stream));
+    RUN(K_ROPE, launch_rope_kv<T>(x_qkv, meta, ck, cv, B, n1, H, Hkv, hd, cap, ctx->inv_freq,
+                                  stream));
+    int nsplit = 1;
+    RUN(K_ATTN, launch_attention<T>(x_qkv, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
+                                    (int)std::min<long long>(ctx->part_cap, 0x7fffffff), B, n1,
+                                    H, Hkv, hd, cap, stream, &nsplit));
+    RUN(K_GEMM_O, launch_gemm<T>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
+                                 ctx->x, stream));
+    RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D, d.rms_eps,
+                                     stream));
+    RUN(K_GEMM_GATE_UP, launch_gemm<T>(EPI_SWIGLU, x_a, (const T *)lw.w_gate_up, R, F, D, x_h,
+                                       nullptr, stream));
+    RUN(K_GEMM_DOWN, launch_gemm<T>(EPI_RESID, x_h, (const T *)lw.w_down, R, D, F, nullptr,
+                                    ctx->x, stream));
+  }
+  RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)w->final_norm, x_a, R, D, d.rms_eps,
+                                   stream));
+  RUN(K_GEMM_LM, launch_gemm<T>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr, logits,
+                                stream));
+  VocabArgs va;
+  va.logits = logits;
+  va.q = draft_q;
+  va.u = uniforms;
+  va.tok = meta.tok;
+  va.par = meta.par;
+  va.n1 = n1;
+  va.tail = 0;
+  va.rows = R;
+  va.V = V;
+  va.k = p->top_k;
+  va.inv_T = 1.0f / p->temperature;
+  va.top_p = p->top_p;
+  va.accept = o->accept;
+  va.resample = o->resample_token;
+  va.bonus = o->bonus_token;
+  va.topk_ids = o->topk_ids;
+  va.topk_probs = o->topk_probs;
+  RUN(K_VOCAB, launch_vocab(va, stream));
+  RUN(K_WALK, launch_walk(meta.tok, meta.par, o->accept, o->resample_token, o->bonus_token, B,
+                          n1, o->acc_prefix_len, o->path, o->path_len, o->next_token,
+                          o->sibling_hit, stream));
+  return ACESPEC_OK;
+}
+
+template <typename T>
+int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
+                     const void *hidden, const int32_t *draft, const float *draft_q,
+                     const float *uniforms, int R, int chain_len, const acespec_params *p,
+                     const acespec_outputs *o, hipStream_t stream) {
+  const acespec_model_desc &d = ctx->d;
+  const int D = d.d_model, V = d.vocab;
+  float *logits = o->logits_out ? o->logits_out : ctx->logits;
+  const T *A = (const T *)hidden;
+  if (final_norm) {
+    RUN(K_RMSNORM, launch_rmsnorm_in<T>((const T *)hidden, (const T *)final_norm, (T *)ctx->a,
+                                        R, D, d.rms_eps, stream));
+    A = (const T *)ctx->a;
+  }
+  RUN(K_GEMM_LM, launch_gemm<T>(EPI_F32, A, (const T *)lm_head, R, V, D, nullptr, logits,
+                                stream));
+  VocabArgs va;
+  va.logits = logits;
+  va.q = draft_q;
+  va.u = uniforms;
+  va.tok = draft;
+  va.par = nullptr;
+  va.n1 = 1;
+  va.tail = 1;
+  va.rows = R;
+  va.V = V;
+  va.k = p->top_k;
+  va.inv_T = 1.0f / p->temperature;
+  va.top_p = p->top_p;
+  va.accept = o->accept;
+  va.resample = o->resample_token;
+  va.bonus = o->bonus_token;
+  va.topk_ids = o->topk_ids;
+  va.topk_probs = o->topk_probs;
+  RUN(K_VOCAB, launch_vocab(va, stream));
+  RUN(K_WALK, launch_walk_tail(o->accept, o->resample_token, draft, R, chain_len, V,
+                               o->acc_prefix_len, o->path, o->path_len, o->next_token,
+                               o->sibling_hit, o->status, stream));
+  return ACESPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *acespec_last_error(void) { return g_err.c_str(); }
+
+int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
+                   acespec_ctx **out) {
+  g_err.clear();
+  if (!desc || !out) return fail(ACESPEC_EINVAL, "desc and out must be non-NULL");
+  *out = nullptr;
+  const acespec_model_desc &d = *desc;
+  if (d.dtype != ACESPEC_F32 && d.dtype != ACESPEC_BF16)
+    return fail(ACESPEC_EINVAL, "unknown dtype %d", (int)d.dtype);
+  if (max_batch < 1 || max_nodes < 0)
+    return fail(ACESPEC_EINVAL, "max_batch >= 1 and max_nodes >= 0 required");
+  if (max_nodes > 64) return fail(ACESPEC_EUNSUPPORTED, "max_nodes > 64 is not supported");
+  if (d.n_layers < 0 || d.d_model < 64 || d.d_model % 64 || d.vocab < 1 || d.vocab % 4 ||
+      d.vocab > 262144)
+    return fail(ACESPEC_EUNSUPPORTED,
+                "need d_model a multiple of 64, vocab a multiple of 4 and <= 262144");
+  if (d.n_layers > 0) {
+    if (d.head_dim != 64 && d.head_dim != 128)
+      return fail(ACESPEC_EUNSUPPORTED, "head_dim must be 64 or 128 (got %d)", d.head_dim);
+    if (d.n_heads < 1 || d.n_kv_heads < 1 || d.n_heads % d.n_kv_heads)
+      return fail(ACESPEC_EINVAL, "n_heads must be a positive multiple of n_kv_heads");
+    if (d.d_ff < 64 || d.d_ff % 64 || (d.n_heads * d.head_dim) % 64)
+      return fail(ACESPEC_EUNSUPPORTED, "d_ff and n_heads*head_dim must be multiples of 64");
+    const int G = d.n_heads / d.n_kv_heads;
+    if ((G * (max_nodes + 1) + 15) / 16 > 32)
+      return fail(ACESPEC_EUNSUPPORTED, "(n_heads/n_kv_heads)*(max_nodes+1) must be <= 512");
+    if (!(d.rope_base > 0.f) || !(d.rms_eps >= 0.f))
+      return fail(ACESPEC_EINVAL, "rope_base > 0 and rms_eps >= 0 required");
+  }
+  acespec_ctx *c = new (std::nothrow) acespec_ctx();
+  if (!c) return fail(ACESPEC_ENOMEM, "host allocation failed");
+  c->d = d;
+  c->max_batch = max_batch;
+  c->max_nodes = max_nodes;
+  c->max_rows = max_batch * (max_nodes + 1);
+  c->esz = d.dtype == ACESPEC_BF16 ? 2 : 4;
+  const size_t R = c->max_rows;
+  const bool layers = d.n_layers > 0;
+  const int G = layers ? d.n_heads / d.n_kv_heads : 1;
+  const size_t QR = (size_t)G * (max_nodes + 1);
+  c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
+  struct Part { size_t bytes; void **dst; };
+  void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
+  void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
+       *p_anc = nullptr, *p_S = nullptr;
+  std::vector<Part> parts = {
+      {R * d.d_model * 4, &p_x},
+      {R * d.d_model * c->esz, &c->a},
+      {layers ? R * d.n_heads * d.head_dim * c->esz : 0, &c->attn},
+      {layers ? R * (d.n_heads + 2 * d.n_kv_heads) * d.head_dim * c->esz : 0, &c->qkv},
+      {layers ? R * d.d_ff * c->esz : 0, &c->h},
+      {R * (size_t)d.vocab * 4, &p_logits},
+      {(size_t)c->part_cap * 4, &p_po},
+      {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
+      {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
+      {R * 4, &p_tok}, {R * 4, &p_par}, {R * 4, &p_pos}, {R * 4, &p_depth}, {R * 8, &p_anc},
+      {(size_t)max_batch * 4, &p_S}};
+  size_t total = 0;
+  for (auto &pt : parts) total += align_up(pt.bytes);
+  if (hipMalloc(&c->ws, total) != hipSuccess) {
+    (void)hipGetLastError();
+    delete c;
+    return fail(ACESPEC_ENOMEM, "hipMalloc of %zu workspace bytes failed", total);
+  }
+  size_t off = 0;
+  for (auto &pt : parts) {
+    *pt.dst = pt.bytes ? (char *)c->ws + off : nullptr;
+    off += align_up(pt.bytes);
+  }
+  c->x = (float *)p_x;
+  c->logits = (float *)p_logits;
+  c->part_o = (float *)p_po;
+  c->part_ml = (float *)p_pml;
+  c->inv_freq = (double *)p_if;
+  c->meta.tok = (int32_t *)p_tok;
+  c->meta.par = (int32_t *)p_par;
+  c->meta.pos = (int32_t *)p_pos;
+  c->meta.depth = (int32_t *)p_depth;
+  c->meta.anc = (uint64_t *)p_anc;
+  c->meta.sess_S = (int32_t *)p_S;
+  if (layers) {
+    std::vector<double> f(d.head_dim / 2);
+    for (int i = 0; i < d.head_dim / 2; ++i)
+      f[i] = std::pow((double)d.rope_base, -2.0 * i / (double)d.head_dim);
+    if (hipMemcpy(c->inv_freq, f.data(), f.size() * 8, hipMemcpyHostToDevice) != hipSuccess) {
+      (void)hipFree(c->ws);
+      delete c;
+      return fail(ACESPEC_EHIP, "copy of the RoPE frequency table failed");
+    }
+  }
+  *out = c;
+  return ACESPEC_OK;
+}
+
+void acespec_destroy(acespec_ctx *c) {
+  if (!c) return;
+  (void)hipDeviceSynchronize();
+  for (auto &r : c->pending) {
+    (void)hipEventDestroy(r.e0);
+    (void)hipEventDestroy(r.e1);
+  }
+  for (auto e : c->free_events) (void)hipEventDestroy(e);
+  (void)hipFree(c->ws);
+  delete c;
+}
+
+int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
+                        const int32_t *tree_tokens, const int32_t *parent_idx,
+                        const float *draft_q, const float *uniforms, int B, int N,
+                        const acespec_params *p, const acespec_outputs *o,
+                        hipStream_t stream) {
+  g_err.clear();
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  const acespec_model_desc &d = ctx->d;
+  if (d.n_layers < 1) return fail(ACESPEC_EINVAL, "context has no layers (tail-only model)");
+  if (!w || !kv || !tree_tokens || !parent_idx || !draft_q || !uniforms)
+    return fail(ACESPEC_EINVAL, "a required pointer is NULL");
+  if (!w->embed || !w->layers || !w->final_norm || !w->lm_head)
+    return fail(ACESPEC_EINVAL, "a weight pointer is NULL");
+  for (int l = 0; l < d.n_layers; ++l) {
+    const acespec_layer_weights &lw = w->layers[l];
+    if (!lw.attn_norm || !lw.wqkv || !lw.wo || !lw.mlp_norm || !lw.w_gate_up || !lw.w_down)
+      return fail(ACESPEC_EINVAL, "layer %d has a NULL weight pointer", l);
+  }
+  if (!kv->k || !kv->v || !kv->prefix_len) return fail(ACESPEC_EINVAL, "kv cache pointer NULL");
+  if (B < 1 || B > ctx->max_batch)
+    return fail(ACESPEC_EINVAL, "B must be in [1, %d] (got %d)", ctx->max_batch, B);
+  if (N < 0 || N > ctx->max_nodes)
+    return fail(N > 64 ? ACESPEC_EUNSUPPORTED : ACESPEC_EINVAL,
+                "N must be in [0, %d] (got %d)", ctx->max_nodes, N);
+  if (kv->capacity < N + 1)
+    return fail(ACESPEC_EINVAL, "kv capacity %d cannot hold the %d tree rows", kv->capacity, N + 1);
+  int rc = check_params(p, d.vocab);
+  if (rc) return rc;
+  rc = check_outputs(o);
+  if (rc) return rc;
+  if (d.dtype == ACESPEC_BF16)
+    return verify_tree_impl<bf16>(ctx, w, kv, tree_tokens, parent_idx, draft_q, uniforms, B, N,
+                                  p, o, stream);
+  return verify_tree_impl<float>(ctx, w, kv, tree_tokens, parent_idx, draft_q, uniforms, B, N,
+                                 p, o, stream);
+}
+
+int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
+                        const void *hidden, const int32_t *draft_tokens, const float *draft_q,
+                        const float *uniforms, int R, int chain_len,
+                        const acespec_params *p, const acespec_outputs *o,
+                        hipStream_t stream) {
+  g_err.clear();
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  if (!lm_head || !hidden || !draft_tokens || !draft_q || !uniforms)
+    return fail(ACESPEC_EINVAL, "a required pointer is NULL");
+  if (R < 1 || R > ctx->max_rows)
+    return fail(ACESPEC_EINVAL, "R must be in [1, %d] (got %d)", ctx->max_rows, R);
+  if (chain_len < 1 || R % chain_len)
+    return fail(ACESPEC_EINVAL, "chain_len must be >= 1 and divide R");
+  int rc = check_params(p, ctx->d.vocab);
+  if (rc) return rc;
+  rc = check_outputs(o);
+  if (rc) return rc;
+  if (ctx->d.dtype == ACESPEC_BF16)
+    return verify_tail_impl<bf16>(ctx, lm_head, final_norm, hidden, draft_tokens, draft_q,
+                                  uniforms, R, chain_len, p, o, stream);
+  return verify_tail_impl<float>(ctx, lm_head, final_norm, hidden, draft_tokens, draft_q,
+                                 uniforms, R, chain_len, p, o, stream);
+}
+
+int acespec_timing_enable(acespec_ctx *ctx, int enable) {
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  ctx->timing = enable != 0;
+  return ACESPEC_OK;
+}
+
+int acespec_timing_read(acespec_ctx *ctx, const char **names, double *total_ms, int *launches,
+                        int max) {
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  for (auto &r : ctx->pending) {
+    if (hipEventSynchronize(r.e1) != hipSuccess) return fail(ACESPEC_EHIP, "event wait failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.e0, r.e1) != hipSuccess)
+      return fail(ACESPEC_EHIP, "hipEventElapsedTime failed");
+    ctx->tot_ms[r.kind] += ms;
+    ctx->launches[r.kind] += 1;
+    ctx->free_events.push_back(r.e0);
+    ctx->free_events.push_back(r.e1);
+  }
+  ctx->pending.clear();
+  int n = 0;
+  for (int k = 0; k < K_COUNT && n < max; ++k) {
+    if (!ctx->launches[k]) continue;
+    if (names) names[n] = kKindNames[k];
+    if (total_ms) total_ms[n] = ctx->tot_ms[k];
+    if (launches) launches[n] = ctx->launches[k];
+    ++n;
+  }
+  for (int k = 0; k < K_COUNT; ++k) {
+    ctx->tot_ms[k] = 0.0;
+    ctx->launches[k] = 0;
+  }
+  return n;
+}
+
+}  // extern "C"

@@ -1,0 +1,134 @@
+// Shared device helpers and the internal launch interface of the verify library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/acespec.h"
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define AS_DEVICE __device__ __forceinline__
+
+template <typename T> AS_DEVICE float to_f32(T v);
+template <> AS_DEVICE float to_f32<float>(float v) { return v; }
+template <> AS_DEVICE float to_f32<bf16>(bf16 v) { return (float)v; }
+
+template <typename T> AS_DEVICE T from_f32(float v);
+template <> AS_DEVICE float from_f32<float>(float v) { return v; }
+template <> AS_DEVICE bf16 from_f32<bf16>(float v) { return (bf16)v; }  // RNE
+
+// Order-preserving map of an fp32 value to uint32 (larger float -> larger key).
+AS_DEVICE uint32_t f32_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+AS_DEVICE float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+AS_DEVICE float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+AS_DEVICE unsigned long long wave_sum_u64(unsigned long long v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+AS_DEVICE int wave_sum_i32(int v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// ------------------------------------------------------------------------------------
+// Tree metadata produced by the tree-prep kernel (one entry per tree row)
+// ------------------------------------------------------------------------------------
+struct TreeMeta {
+  int32_t *tok;      // [rows] token id, clamped into [0, V)
+  int32_t *par;      // [rows] parent row within the session (-1 for the root); a chain
+                     //        for sessions whose tree is malformed
+  int32_t *pos;      // [rows] RoPE position = prefix_len + depth
+  int32_t *depth;    // [rows]
+  uint64_t *anc;     // [rows] bit (j-1) set iff drafted row j is r or an ancestor of r
+  int32_t *sess_S;   // [B] prefix length, clamped so that S + N + 1 <= capacity
+};
+
+// Fixed-point scale for deterministic mass sums in the vocabulary kernel.
+#define AS_FX_SCALE 1099511627776.0f  /* 2^40 */
+
+// ------------------------------------------------------------------------------------
+// Launchers (defined in the kernel translation units)
+// ------------------------------------------------------------------------------------
+namespace acespec {
+
+hipError_t launch_tree_prep(const int32_t *tokens, const int32_t *parents,
+                            const int32_t *prefix_len, int B, int n1, int V, int capacity,
+                            TreeMeta meta, int32_t *status, hipStream_t s);
+
+template <typename T>
+hipError_t launch_embed(const T *embed, const int32_t *tok, float *x, int rows, int d,
+                        hipStream_t s);
+
+template <typename T>
+hipError_t launch_rmsnorm(const float *x, const T *gain, T *out, int rows, int d, float eps,
+                          hipStream_t s);
+
+// Same, for inputs already in the model dtype (LM-head tail).
+template <typename T>
+hipError_t launch_rmsnorm_in(const T *x, const T *gain, T *out, int rows, int d, float eps,
+                             hipStream_t s);
+
+template <typename T>
+hipError_t launch_rope_kv(T *qkv, const TreeMeta &meta, T *cache_k, T *cache_v,
+                          int B, int n1, int H, int Hkv, int hd, int capacity,
+                          const double *inv_freq, hipStream_t s);
+
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
+
+// C[M, N] = A[M, K] . W[N, K]^T with the epilogue:
+//  EPI_STORE : out (model dtype) [M, N]
+//  EPI_RESID : resid (fp32) [M, N] += C
+//  EPI_SWIGLU: W holds 2F rows (gate, up); out[M, F] = silu(gate) * up, N = F
+//  EPI_F32   : outf (fp32) [M, N] = C
+template <typename T>
+hipError_t launch_gemm(int epi, const T *A, const T *W, int M, int N, int K, T *out,
+                       float *outf, hipStream_t s);
+
+template <typename T>
+hipError_t launch_attention(const T *qkv, const T *cache_k, const T *cache_v,
+                            const TreeMeta &meta, T *out, float *part_o, float *part_ml,
+                            int part_capacity, int B, int n1, int H, int Hkv, int hd,
+                            int capacity, hipStream_t s, int *nsplit_used);
+
+struct VocabArgs {
+  const float *logits;      // [rows, V]
+  const float *q;           // [rows, V]
+  const float *u;           // [rows, 3]
+  const int32_t *tok;       // [rows] token of each row (children look theirs up here)
+  const int32_t *par;       // [rows] parent row within the session, -1 for the root
+  int n1;                   // rows per session (1 for the tail)
+  int tail;                 // 1: each row is the parent of one drafted token tok[row]
+  int rows, V, k;
+  float inv_T, top_p;
+  uint8_t *accept;
+  int32_t *resample;
+  int32_t *bonus;
+  int32_t *topk_ids;
+  float *topk_probs;
+};
+hipError_t launch_vocab(const VocabArgs &a, hipStream_t s);
+
+hipError_t launch_walk(const int32_t *tok, const int32_t *par, const uint8_t *accept,
+                       const int32_t *resample, const int32_t *bonus, int B, int n1,
+                       int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
+                       int32_t *next_token, uint8_t *sibling_hit, hipStream_t s);
+
+hipError_t launch_walk_tail(const uint8_t *accept, const int32_t *resample,
+                            const int32_t *draft, int R, int chain_len, int V,
+                            int32_t *acc_prefix_len, int32_t *path,
+                            int32_t *path_len, int32_t *next_token, uint8_t *sibling_hit,
+                            int32_t *status, hipStream_t s);
+
+}  // namespace acespec

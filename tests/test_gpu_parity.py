@@ -1,0 +1,235 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on the same
+seeded inputs.  Logits are compared element by element; decisions are compared with the
+oracle's verify stage run on the GPU's own logits, every mismatch classified."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import model as om
+from oracle import verify as ov
+from tests import harness as hz
+
+pytestmark = pytest.mark.gpu
+
+
+def small_bf16(**kw):
+    base = dict(name="small-bf16", dtype="bf16", L=2, d=320, H=8, Hkv=2, hd=64, F=576, V=5000,
+                B=3, S=150, tree="widths_2455", depth=4, q_std=2.5, q_T=0.8, T=0.8,
+                top_p=0.9, top_k=24, ragged=True, random_gains=True, seed_base=4242)
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+def _logits_rows(run, z_ref):
+    """GPU logits of the sampled sessions, row-indexed like the outputs."""
+    n1 = run.host_in["tokens"].shape[1]
+    zg = run.outs["logits_out"]
+    rows = {}
+    for i, b in enumerate(run.sessions):
+        for r in range(n1):
+            rows[b * n1 + r] = zg[b * n1 + r].numpy().astype(np.float64)
+    return rows
+
+
+def _check_tree(run, tol):
+    z_ref = hz.oracle_tree_logits(run)
+    n1 = run.host_in["tokens"].shape[1]
+    zg = np.stack([run.outs["logits_out"][b * n1:(b + 1) * n1].numpy() for b in run.sessions])
+    err = hz.logits_rel_err(zg.astype(np.float64), z_ref)
+    hz.log(f"logits max rel err {err.max():.3e} (tol {tol})")
+    assert err.max() <= tol, err.max()
+    rep = hz.check_tree_decisions(run, _logits_rows(run, z_ref))
+    hz.log(f"decisions: {rep}")
+    assert rep.ok(), str(rep)
+    return err, rep
+
+
+def test_tree_tiny_fp32_full_config():
+    """The tiny fp32 workload at its full size (2 layers, d=256, vocab 4096, 8-node tree)."""
+    w = synth.get("tiny-fp32")
+    run = hz.run_tree(w)
+    _check_tree(run, tol=1e-4)
+
+
+@pytest.mark.parametrize("variant", [
+    dict(),                                                    # hd 64, G 4, 16-node tree
+    dict(hd=128, H=4, Hkv=1, d=256, tree="chain_sib", depth=6, sib=2, V=4100),
+    dict(hd=128, H=8, Hkv=8, tree="chain", depth=9, B=2, S=64, ragged=False, V=2048),
+    dict(hd=64, H=8, Hkv=2, tree="chain_sib", depth=8, sib=7, B=2, S=700, top_k=64),
+])
+def test_tree_small_bf16(variant):
+    w = small_bf16(**variant)
+    run = hz.run_tree(w)
+    _check_tree(run, tol=2e-2)
+
+
+def test_tree_empty_tree_and_long_ragged_prefix():
+    """N = 0 (root only: bonus and top-k only) and prefixes that end mid-chunk."""
+    w = small_bf16(tree="chain", depth=0, B=5, S=1000, ragged=True)
+    run = hz.run_tree(w)
+    _check_tree(run, tol=2e-2)
+    assert run.outs["path_len"].tolist() == [0] * 5
+
+
+def test_tree_1b_full_size_sampled_sessions():
+    w = synth.get("1b-bf16")
+    run = hz.run_tree(w, sessions=[0, 9, 15])
+    _check_tree(run, tol=2e-2)
+
+
+@pytest.mark.timeout(900)
+def test_tree_8b_full_size_sampled_session():
+    w = synth.get("8b-bf16")
+    run = hz.run_tree(w, sessions=[37])
+    _check_tree(run, tol=2e-2)
+
+
+@pytest.mark.timeout(900)
+def test_tree_8b_long_wide_sampled_session():
+    w = synth.get("8b-long-wide")
+    run = hz.run_tree(w, sessions=[5])
+    _check_tree(run, tol=2e-2)
+
+
+# ---------------------------------------------------------------------------------------
+# LM-head tail
+# ---------------------------------------------------------------------------------------
+
+
+def _run_tail(w, W=None, rows_check=None, tol=1e-4):
+    from paper_2609_02514_amd.acespec import Verifier
+    dev = "cuda"
+    W = W or synth.make_weights(w, dev)
+    batch = synth.make_batch(w, dev, weights=W)
+    R = w.rows
+    q_h, u_h, d_h = hz.host(batch.q), hz.host(batch.u), hz.host(batch.draft_tokens)
+    v = Verifier.for_workload(w)
+    outs = v.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, dev, True)
+    hz.log(f"verify_tail R={R} V={w.V}")
+    v.verify_tail(W.lm_head, None, batch.hidden, batch.draft_tokens, batch.q, batch.u,
+                  w.chain_len, w.T, w.top_p, w.top_k, outs)
+    torch.cuda.synchronize()
+    g = {k: (hz.host(t) if t is not None else None) for k, t in outs.items()}
+    v.close()
+    rows = list(range(R)) if rows_check is None else rows_check
+    z_ref = om.lm_head_tail(W, batch.hidden[rows])
+    zg = g["logits_out"][rows].numpy().astype(np.float64)
+    err = hz.logits_rel_err(zg, z_ref)
+    hz.log(f"tail logits max rel err {err.max():.3e}")
+    assert err.max() <= tol
+    rep = hz.Report()
+    for i, r in enumerate(rows):
+        z = zg[i]
+        qr = q_h[r].numpy().astype(np.float64)
+        u = u_h[r].numpy().astype(np.float64)
+        hz.compare_row_decisions(rep, f"r{r}", z, qr, [r], None, u, w.T, w.top_p, w.top_k, g, r,
+                                 {})
+        hz.compare_child(rep, f"c{r}", z, qr, int(d_h[r]), float(u[0]), float(u[1]), w.T,
+                         w.top_p, int(g["accept"][r]), int(g["resample_token"][r]))
+    hz.log(f"tail decisions: {rep}")
+    assert rep.ok(), str(rep)
+    # chain walk from the GPU's own accept bits
+    pl, nx = ov.walk_tail(g["accept"].numpy(), g["resample_token"].numpy(), w.chain_len)
+    assert g["path_len"].tolist() == pl.tolist()
+    assert g["next_token"].tolist() == nx.tolist()
+    assert g["status"].tolist() == [0] * (R // w.chain_len)
+    return g
+
+
+def test_tail_small():
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-small", d=256, V=5004, rows=96,
+                                          chain_len=8, top_k=16)
+    _run_tail(w)
+
+
+def test_tail_exact_logit_ties():
+    """Duplicated LM-head rows give exactly equal logits: ties must be broken by token id
+    in the nucleus, the top-k payload and the inverse CDFs."""
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-ties", d=128, V=4096, rows=64,
+                                          chain_len=4, top_k=32, T=1.0, top_p=0.5)
+    W = synth.make_weights(w, "cuda")
+    W.lm_head = W.lm_head[torch.arange(w.V, device="cuda") // 8].contiguous()
+    _run_tail(w, W=W)
+
+
+@pytest.mark.timeout(900)
+def test_tail_8b_full_size_sampled_rows():
+    w = synth.get("8b-lmhead-tail")
+    rng = np.random.default_rng(0)
+    rows = sorted(rng.choice(w.rows, 48, replace=False).tolist())
+    g = _run_tail(w, rows_check=rows, tol=1e-4)
+    rate = float(g["accept"].float().mean())
+    hz.log(f"tail acceptance rate {rate:.3f}")
+    assert 0.3 < rate < 0.95
+
+
+# ---------------------------------------------------------------------------------------
+# ABI behaviour on the device
+# ---------------------------------------------------------------------------------------
+
+
+def test_bad_trees_flag_only_their_session():
+    from paper_2609_02514_amd.acespec import Verifier
+    w = small_bf16(B=4, ragged=False)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda")
+    par = batch.parents.clone()
+    tok = batch.tokens.clone()
+    par[1, 5] = 7          # forward reference
+    tok[2, 3] = w.V + 3    # token outside the vocabulary
+    plen = batch.prefix_len.clone()
+    plen[3] = batch.cap    # prefix leaves no room for the tree
+    v = Verifier.for_workload(w)
+    B, n1 = tok.shape
+    outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)
+    v.verify_tree(v.weights_struct(W), batch.kv_k, batch.kv_v, batch.cap, plen, tok, par,
+                  batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
+    torch.cuda.synchronize()
+    assert outs["status"].tolist() == [0, -5, -5, -5]
+    v.close()
+
+
+def test_argument_errors_are_synchronous():
+    from paper_2609_02514_amd import acespec as A
+    w = small_bf16(B=2)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda")
+    v = A.Verifier.for_workload(w)
+    B, n1 = batch.tokens.shape
+    outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)
+    ws = v.weights_struct(W)
+    for T, top_p, k, code in [(0.0, 0.9, 8, -1), (0.8, 0.0, 8, -1), (0.8, 1.5, 8, -1),
+                              (0.8, 0.9, 0, -1), (0.8, 0.9, 300, -1)]:
+        with pytest.raises(A.AcespecError) as e:
+            v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len,
+                          batch.tokens, batch.parents, batch.q, batch.u, T, top_p, k, outs)
+        assert e.value.code == code
+    with pytest.raises(A.AcespecError):   # more sessions than the context holds
+        big = batch.tokens.repeat(3, 1)
+        v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, big,
+                      batch.parents.repeat(3, 1), batch.q, batch.u, 0.8, 0.9, 8, outs)
+    v.close()
+    with pytest.raises(A.AcespecError) as e:
+        A.Verifier(1, 256, 4, 4, 96, 512, 1000, "bf16", 2, 4)   # head_dim 96
+    assert e.value.code == -2
+
+
+def test_run_to_run_bitwise_determinism():
+    from paper_2609_02514_amd.acespec import Verifier
+    w = small_bf16(B=2)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda")
+    v = Verifier.for_workload(w)
+    B, n1 = batch.tokens.shape
+    ws = v.weights_struct(W)
+    res = []
+    for _ in range(2):
+        outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", True)
+        v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
+                      batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
+        torch.cuda.synchronize()
+        res.append({k: t.clone() for k, t in outs.items() if t is not None})
+    for k in res[0]:
+        assert torch.equal(res[0][k], res[1][k]), k
+    v.close()
