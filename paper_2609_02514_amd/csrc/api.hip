@@ -51,7 +51,8 @@ struct acespec_ctx {
   size_t esz = 0;  // bytes per model-dtype element
   void *ws = nullptr;
   float *x = nullptr, *logits = nullptr, *part_o = nullptr, *part_ml = nullptr;
-  void *a = nullptr, *attn = nullptr, *qkv = nullptr, *h = nullptr;
+  void *a = nullptr, *attn = nullptr, *q = nullptr, *h = nullptr;  // activation type
+  float *qkv = nullptr;                                              // fp32 projection
   long long part_cap = 0;
   double *inv_freq = nullptr;
   TreeMeta meta{};
@@ -128,12 +129,13 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
                      const int32_t *tokens, const int32_t *parents, const float *draft_q,
                      const float *uniforms, int B, int N, const acespec_params *p,
                      const acespec_outputs *o, hipStream_t stream) {
+  typedef typename ActOf<T>::type A;
   const acespec_model_desc &d = ctx->d;
   const int n1 = N + 1, R = B * n1;
   const int L = d.n_layers, D = d.d_model, H = d.n_heads, Hkv = d.n_kv_heads, hd = d.head_dim;
   const int F = d.d_ff, V = d.vocab, QKVN = (H + 2 * Hkv) * hd;
   const int cap = kv->capacity;
-  T *x_a = (T *)ctx->a, *x_attn = (T *)ctx->attn, *x_qkv = (T *)ctx->qkv, *x_h = (T *)ctx->h;
+  A *x_a = (A *)ctx->a, *x_attn = (A *)ctx->attn, *x_q = (A *)ctx->q, *x_h = (A *)ctx->h;
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
   const TreeMeta &meta = ctx->meta;
 
@@ -145,29 +147,28 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
     const acespec_layer_weights &lw = w->layers[l];
     T *ck = (T *)kv->k + l * layer_stride;
     T *cv = (T *)kv->v + l * layer_stride;
-    RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)lw.attn_norm, x_a, R, D, d.rms_eps,
-                                     stream));
-    RUN(K_GEMM_QKV, launch_gemm<T>(EPI_STORE, x_a, (const T *)lw.wqkv, R, QKVN, D, x_qkv,
-                                   nullptr, stream));
-    RUN(K_ROPE, launch_rope_kv<T>(x_qkv, meta, ck, cv, B, n1, H, Hkv, hd, cap, ctx->inv_freq,
-                                  stream));
+    RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.attn_norm, x_a, R, D,
+                                             d.rms_eps, stream)));
+    RUN(K_GEMM_QKV, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)lw.wqkv, R, QKVN, D, nullptr,
+                                       ctx->qkv, stream)));
+    RUN(K_ROPE, launch_rope_kv<T>(ctx->qkv, x_q, meta, ck, cv, B, n1, H, Hkv, hd, cap,
+                                  ctx->inv_freq, stream));
     int nsplit = 1;
-    RUN(K_ATTN, launch_attention<T>(x_qkv, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
-                                    (int)std::min<long long>(ctx->part_cap, 0x7fffffff), B, n1,
-                                    H, Hkv, hd, cap, stream, &nsplit));
-    RUN(K_GEMM_O, launch_gemm<T>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
-                                 ctx->x, stream));
-    RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D, d.rms_eps,
-                                     stream));
-    RUN(K_GEMM_GATE_UP, launch_gemm<T>(EPI_SWIGLU, x_a, (const T *)lw.w_gate_up, R, F, D, x_h,
-                                       nullptr, stream));
-    RUN(K_GEMM_DOWN, launch_gemm<T>(EPI_RESID, x_h, (const T *)lw.w_down, R, D, F, nullptr,
-                                    ctx->x, stream));
+    RUN(K_ATTN, launch_attention<T>(x_q, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
+                                    ctx->part_cap, B, n1, H, Hkv, hd, cap, stream, &nsplit));
+    RUN(K_GEMM_O, (launch_gemm<T, A>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
+                                     ctx->x, stream)));
+    RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D,
+                                             d.rms_eps, stream)));
+    RUN(K_GEMM_GATE_UP, (launch_gemm<T, A>(EPI_SWIGLU, x_a, (const T *)lw.w_gate_up, R, F, D,
+                                           x_h, nullptr, stream)));
+    RUN(K_GEMM_DOWN, (launch_gemm<T, A>(EPI_RESID, x_h, (const T *)lw.w_down, R, D, F, nullptr,
+                                        ctx->x, stream)));
   }
-  RUN(K_RMSNORM, launch_rmsnorm<T>(ctx->x, (const T *)w->final_norm, x_a, R, D, d.rms_eps,
-                                   stream));
-  RUN(K_GEMM_LM, launch_gemm<T>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr, logits,
-                                stream));
+  RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)w->final_norm, x_a, R, D,
+                                           d.rms_eps, stream)));
+  RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr,
+                                    logits, stream)));
   VocabArgs va;
   va.logits = logits;
   va.q = draft_q;
@@ -198,17 +199,19 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
                      const void *hidden, const int32_t *draft, const float *draft_q,
                      const float *uniforms, int R, int chain_len, const acespec_params *p,
                      const acespec_outputs *o, hipStream_t stream) {
+  typedef typename ActOf<T>::type A;
   const acespec_model_desc &d = ctx->d;
   const int D = d.d_model, V = d.vocab;
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
-  const T *A = (const T *)hidden;
   if (final_norm) {
-    RUN(K_RMSNORM, launch_rmsnorm_in<T>((const T *)hidden, (const T *)final_norm, (T *)ctx->a,
-                                        R, D, d.rms_eps, stream));
-    A = (const T *)ctx->a;
+    RUN(K_RMSNORM, (launch_rmsnorm<T, T>((const T *)hidden, (const T *)final_norm, (A *)ctx->a,
+                                         R, D, d.rms_eps, stream)));
+    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)ctx->a, (const T *)lm_head, R, V, D,
+                                      nullptr, logits, stream)));
+  } else {
+    RUN(K_GEMM_LM, (launch_gemm<T, T>(EPI_F32, (const T *)hidden, (const T *)lm_head, R, V, D,
+                                      nullptr, logits, stream)));
   }
-  RUN(K_GEMM_LM, launch_gemm<T>(EPI_F32, A, (const T *)lm_head, R, V, D, nullptr, logits,
-                                stream));
   VocabArgs va;
   va.logits = logits;
   va.q = draft_q;
@@ -274,7 +277,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->max_batch = max_batch;
   c->max_nodes = max_nodes;
   c->max_rows = max_batch * (max_nodes + 1);
-  c->esz = d.dtype == ACESPEC_BF16 ? 2 : 4;
+  c->esz = d.dtype == ACESPEC_BF16 ? 2 : 4;  // bytes per activation (fp16 or fp32)
   const size_t R = c->max_rows;
   const bool layers = d.n_layers > 0;
   const int G = layers ? d.n_heads / d.n_kv_heads : 1;
@@ -282,13 +285,15 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
+  void *p_qkv = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
       {R * d.d_model * 4, &p_x},
       {R * d.d_model * c->esz, &c->a},
       {layers ? R * d.n_heads * d.head_dim * c->esz : 0, &c->attn},
-      {layers ? R * (d.n_heads + 2 * d.n_kv_heads) * d.head_dim * c->esz : 0, &c->qkv},
+      {layers ? R * (d.n_heads + 2 * d.n_kv_heads) * d.head_dim * 4 : 0, &p_qkv},
+      {layers ? R * d.n_heads * d.head_dim * c->esz : 0, &c->q},
       {layers ? R * d.d_ff * c->esz : 0, &c->h},
       {R * (size_t)d.vocab * 4, &p_logits},
       {(size_t)c->part_cap * 4, &p_po},
@@ -309,6 +314,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
     off += align_up(pt.bytes);
   }
   c->x = (float *)p_x;
+  c->qkv = (float *)p_qkv;
   c->logits = (float *)p_logits;
   c->part_o = (float *)p_po;
   c->part_ml = (float *)p_pml;

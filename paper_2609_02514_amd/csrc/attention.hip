@@ -6,14 +6,16 @@
 // values of tree row j sit in cache slot prefix_len + j, so one contiguous key range
 // [0, prefix_len + N + 1) covers everything and the mask applies to its tail only.
 //
-// bf16 kernel: one workgroup per (split, kv head, session).  The G query heads of the
+// bf16 model: one workgroup per (split, kv head, session).  The G query heads of the
 // kv head times the N+1 tree rows form the query rows (row = tree_row * G + head), in
 // 16-row MFMA tiles spread over the workgroup's waves.  The key range of the split is
 // streamed in 64-key chunks with coalesced 16-byte loads into LDS (keys XOR-swizzled,
-// values with a padded row stride); the next chunk's loads are in flight while the
-// current chunk is processed.  S = Q K^T and O += P V use v_mfma_f32_16x16x32_bf16 with
-// fp32 accumulation and an online softmax in base 2.  P goes through a per-wave LDS
-// tile to become an MFMA operand.  With several splits, unnormalised partial outputs
+// values with a padded row stride), converted from the bf16 cache to fp16 on the way
+// (exact in the fp16 normal range); the next chunk's loads are in flight while the
+// current chunk is processed.  Queries arrive in fp16.  S = Q K^T and O += P V use
+// v_mfma_f32_16x16x32_f16 with fp32 accumulation and an online softmax in base 2; P
+// (in [0, 1]) is rounded to fp16 and goes through a per-wave LDS tile to become an MFMA
+// operand.  With several splits, unnormalised partial outputs
 // and (max, sum) pairs are merged by a small combine kernel.
 //
 // fp32 kernel (tiny models): one wave per (tree row, query head), keys in sequence.
@@ -26,9 +28,9 @@ constexpr float LOG2E = 1.4426950408889634f;
 
 template <int HD>
 struct AttnSmem {
-  static constexpr int VSTRIDE = HD + 2;                   // bf16 elements per V row
-  bf16 k[KC * HD];
-  bf16 v[KC * VSTRIDE];
+  static constexpr int VSTRIDE = HD + 2;                   // fp16 elements per V row
+  f16 k[KC * HD];
+  f16 v[KC * VSTRIDE];
 };
 
 template <int HD>
@@ -46,14 +48,14 @@ AS_DEVICE bool tree_visible(int slot, int S, int n1, uint64_t anc) {
 constexpr int NWAVES = 8;  // waves per workgroup (tiles are dealt to them in order)
 
 template <int HD, int TPW>
-__global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
-    const bf16 *__restrict__ qkv, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
-    TreeMeta meta, bf16 *__restrict__ out, float *__restrict__ part_o,
+__global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
+    const f16 *__restrict__ qin, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
+    TreeMeta meta, f16 *__restrict__ out, float *__restrict__ part_o,
     float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit) {
   constexpr int KSTEPS = HD / 32, NB = HD / 16, PSTRIDE = KC + 8;
   constexpr int VST = AttnSmem<HD>::VSTRIDE;
   __shared__ __attribute__((aligned(16))) AttnSmem<HD> sm;
-  __shared__ __attribute__((aligned(16))) bf16 sP[NWAVES][16 * PSTRIDE];
+  __shared__ __attribute__((aligned(16))) f16 sP[NWAVES][16 * PSTRIDE];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int G = H / Hkv, QR = G * n1;
@@ -69,11 +71,11 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
   const int c_end = min(nchunks, c_begin + cps);
   const size_t kvbase = ((size_t)b * Hkv + g) * capacity * HD;
   const size_t row0 = (size_t)b * n1;
-  const int qkv_stride = (H + 2 * Hkv) * HD;
+  const int q_stride = H * HD;
   const float sscale = LOG2E / sqrtf((float)HD);
 
   // Query fragments (A operand of S = Q K^T) and running softmax state.
-  bf16x8 qf[TPW][KSTEPS];
+  f16x8 qf[TPW][KSTEPS];
   f32x4 o[TPW][NB];
   float m_run[TPW][4], l_run[TPW][4];
 #pragma unroll
@@ -82,9 +84,9 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
     int qi = tile * 16 + lr;
     qi = qi < QR ? qi : QR - 1;
     const int r = qi / G, h = g * G + (qi - r * G);
-    const bf16 *qp = qkv + (row0 + r) * qkv_stride + h * HD;
+    const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) qf[t][s] = *(const bf16x8 *)(qp + s * 32 + lk * 8);
+    for (int s = 0; s < KSTEPS; ++s) qf[t][s] = *(const f16x8 *)(qp + s * 32 + lk * 8);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       m_run[t][e] = -INFINITY;
@@ -115,9 +117,10 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + i * NWAVES * 64;
       const int key = p / (HD / 8), ch = p - key * (HD / 8);
-      *(bf16x8 *)(&sm.k[kswz<HD>(key, ch)]) = rk[i];
+      *(f16x8 *)(&sm.k[kswz<HD>(key, ch)]) = bf16x8_to_f16x8(rk[i]);
+      const f16x8 v16 = bf16x8_to_f16x8(rv[i]);
       uint32_t *vd = (uint32_t *)(&sm.v[key * VST + ch * 8]);
-      const uint32_t *vs = (const uint32_t *)(&rv[i]);
+      const uint32_t *vs = (const uint32_t *)(&v16);
       vd[0] = vs[0];
       vd[1] = vs[1];
       vd[2] = vs[2];
@@ -126,7 +129,7 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
   };
 
   if (c_begin < c_end) load_chunk(c_begin);
-  bf16 *myP = sP[wave];
+  f16 *myP = sP[wave];
   for (int c = c_begin; c < c_end; ++c) {
     __syncthreads();  // previous chunk fully consumed
     store_chunk();
@@ -147,8 +150,8 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
         sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < KSTEPS; ++s) {
-          const bf16x8 kf = *(const bf16x8 *)(&sm.k[kswz<HD>(kb * 16 + lr, s * 4 + lk)]);
-          sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[t][s], kf, sc[kb], 0, 0, 0);
+          const f16x8 kf = *(const f16x8 *)(&sm.k[kswz<HD>(kb * 16 + lr, s * 4 + lk)]);
+          sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qf[t][s], kf, sc[kb], 0, 0, 0);
         }
       }
       // Scale, mask (tree slots only), running max.  sc[kb][e] is the score of query row
@@ -192,7 +195,7 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
       for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bf16 pb = (bf16)exp2f(sc[kb][e] - mref[e]);
+          const f16 pb = (f16)exp2f(sc[kb][e] - mref[e]);
           rs[e] += (float)pb;
           myP[(lk * 4 + e) * PSTRIDE + kb * 16 + lr] = pb;
         }
@@ -215,14 +218,14 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
       // O += P V over two k-steps of 32 keys.  Both operands use key = s2*32 + lk*8 + j.
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const bf16x8 pa = *(const bf16x8 *)(&myP[lr * PSTRIDE + s2 * 32 + lk * 8]);
+        const f16x8 pa = *(const f16x8 *)(&myP[lr * PSTRIDE + s2 * 32 + lk * 8]);
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          bf16x8 vb;
-          const bf16 *vcol = &sm.v[(s2 * 32 + lk * 8) * VST + nb * 16 + lr];
+          f16x8 vb;
+          const f16 *vcol = &sm.v[(s2 * 32 + lk * 8) * VST + nb * 16 + lr];
 #pragma unroll
           for (int j = 0; j < 8; ++j) vb[j] = vcol[j * VST];
-          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[t][nb], 0, 0, 0);
+          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o[t][nb], 0, 0, 0);
         }
       }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -242,9 +245,9 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_bf16_kernel(
       const int r = qi / G, h = g * G + (qi - r * G);
       if (nsplit == 1) {
         const float inv = l_run[t][e] > 0.f ? 1.0f / l_run[t][e] : 0.f;
-        bf16 *op = out + (row0 + r) * (size_t)(H * HD) + h * HD;
+        f16 *op = out + (row0 + r) * (size_t)(H * HD) + h * HD;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) op[nb * 16 + lr] = (bf16)(o[t][nb][e] * inv);
+        for (int nb = 0; nb < NB; ++nb) op[nb * 16 + lr] = (f16)(o[t][nb][e] * inv);
       } else {
         const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
         float *po = part_o + (item * QR + qi) * HD;
@@ -286,14 +289,14 @@ __global__ void attn_combine_kernel(const float *__restrict__ part_o,
 
 // fp32 path: one wave per (tree row, query head); lane i owns dims i and i + 64.
 __global__ __launch_bounds__(64) void tree_attn_f32_kernel(
-    const float *__restrict__ qkv, const float *__restrict__ ck, const float *__restrict__ cv,
+    const float *__restrict__ qin, const float *__restrict__ ck, const float *__restrict__ cv,
     TreeMeta meta, float *__restrict__ out, int n1, int H, int Hkv, int HD, int capacity) {
   const int h = blockIdx.x, row = blockIdx.y;
   const int b = row / n1;
   const int G = H / Hkv, g = h / G, lane = threadIdx.x;
   const int S = meta.sess_S[b];
   const uint64_t anc = meta.anc[row];
-  const float *q = qkv + (size_t)row * (H + 2 * Hkv) * HD + h * HD;
+  const float *q = qin + (size_t)row * H * HD + h * HD;
   const float q0 = lane < HD ? q[lane] : 0.f, q1 = lane + 64 < HD ? q[lane + 64] : 0.f;
   const size_t kvbase = ((size_t)b * Hkv + g) * capacity * HD;
   const float scale = 1.0f / sqrtf((float)HD);
@@ -317,10 +320,10 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(
 }
 
 template <int HD, int TPW>
-void launch_bf16(dim3 grid, hipStream_t s, const bf16 *qkv, const bf16 *ck,
-                 const bf16 *cv, const TreeMeta &meta, bf16 *out, float *po, float *pml, int n1,
-                 int H, int Hkv, int capacity, int nsplit) {
-  hipLaunchKernelGGL((tree_attn_bf16_kernel<HD, TPW>), grid, dim3(NWAVES * 64), 0, s, qkv, ck, cv,
+void launch_mfma(dim3 grid, hipStream_t s, const f16 *q, const bf16 *ck, const bf16 *cv,
+                 const TreeMeta &meta, f16 *out, float *po, float *pml, int n1, int H, int Hkv,
+                 int capacity, int nsplit) {
+  hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, TPW>), grid, dim3(NWAVES * 64), 0, s, q, ck, cv,
                      meta, out, po, pml, n1, H, Hkv, capacity, nsplit);
 }
 
@@ -329,9 +332,9 @@ void launch_bf16(dim3 grid, hipStream_t s, const bf16 *qkv, const bf16 *ck,
 namespace acespec {
 
 template <>
-hipError_t launch_attention<bf16>(const bf16 *qkv, const bf16 *ck, const bf16 *cv,
-                                  const TreeMeta &meta, bf16 *out, float *part_o,
-                                  float *part_ml, int part_capacity, int B, int n1, int H,
+hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
+                                  const TreeMeta &meta, f16 *out, float *part_o,
+                                  float *part_ml, long long part_capacity, int B, int n1, int H,
                                   int Hkv, int hd, int capacity, hipStream_t s,
                                   int *nsplit_used) {
   const int G = H / Hkv, QR = G * n1;
@@ -348,8 +351,8 @@ hipError_t launch_attention<bf16>(const bf16 *qkv, const bf16 *ck, const bf16 *c
   while (nsplit > 1 && (long long)items * nsplit * QR * hd > part_capacity) --nsplit;
   *nsplit_used = nsplit;
   const dim3 grid(nsplit, Hkv, B);
-#define GO(HD_, TPW_)                                                                      \
-  launch_bf16<HD_, TPW_>(grid, s, qkv, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv, \
+#define GO(HD_, TPW_)                                                                     \
+  launch_mfma<HD_, TPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,      \
                          capacity, nsplit)
   if (hd == 128) {
     if (tpw == 1) GO(128, 1); else if (tpw == 2) GO(128, 2); else if (tpw == 3) GO(128, 3); else GO(128, 4);
@@ -359,18 +362,18 @@ hipError_t launch_attention<bf16>(const bf16 *qkv, const bf16 *ck, const bf16 *c
 #undef GO
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nsplit == 1) return e;
-  hipLaunchKernelGGL(attn_combine_kernel<bf16>, dim3(Hkv, B), dim3(256), 0, s, part_o, part_ml,
+  hipLaunchKernelGGL(attn_combine_kernel<f16>, dim3(Hkv, B), dim3(256), 0, s, part_o, part_ml,
                      out, n1, H, Hkv, hd, nsplit);
   return hipGetLastError();
 }
 
 template <>
-hipError_t launch_attention<float>(const float *qkv, const float *ck, const float *cv,
-                                   const TreeMeta &meta, float *out, float *, float *, int,
-                                   int B, int n1, int H, int Hkv, int hd, int capacity,
-                                   hipStream_t s, int *nsplit_used) {
+hipError_t launch_attention<float>(const float *q, const float *ck, const float *cv,
+                                   const TreeMeta &meta, float *out, float *, float *,
+                                   long long, int B, int n1, int H, int Hkv, int hd,
+                                   int capacity, hipStream_t s, int *nsplit_used) {
   *nsplit_used = 1;
-  hipLaunchKernelGGL(tree_attn_f32_kernel, dim3(H, B * n1), dim3(64), 0, s, qkv, ck, cv, meta,
+  hipLaunchKernelGGL(tree_attn_f32_kernel, dim3(H, B * n1), dim3(64), 0, s, q, ck, cv, meta,
                      out, n1, H, Hkv, hd, capacity);
   return hipGetLastError();
 }

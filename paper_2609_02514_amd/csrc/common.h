@@ -6,18 +6,37 @@
 #include "../../include/acespec.h"
 
 typedef __bf16 bf16;
+typedef _Float16 f16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Storage of a bf16 model: weights and KV cache in bf16; activations handed from one
+// kernel to the next in fp16 (same MFMA rate on gfx950, 3 more mantissa bits: the
+// rounding of activations is what dominates the logit error of a deep bf16 decoder).
+// An fp32 model keeps everything in fp32.
+template <typename TW> struct ActOf { typedef f16 type; };
+template <> struct ActOf<float> { typedef float type; };
 
 #define AS_DEVICE __device__ __forceinline__
 
 template <typename T> AS_DEVICE float to_f32(T v);
 template <> AS_DEVICE float to_f32<float>(float v) { return v; }
 template <> AS_DEVICE float to_f32<bf16>(bf16 v) { return (float)v; }
+template <> AS_DEVICE float to_f32<f16>(f16 v) { return (float)v; }
 
 template <typename T> AS_DEVICE T from_f32(float v);
 template <> AS_DEVICE float from_f32<float>(float v) { return v; }
 template <> AS_DEVICE bf16 from_f32<bf16>(float v) { return (bf16)v; }  // RNE
+template <> AS_DEVICE f16 from_f32<f16>(float v) { return (f16)v; }     // RNE
+
+// Exact for values in the fp16 normal range (bf16 has 8 significant bits, fp16 11).
+AS_DEVICE f16x8 bf16x8_to_f16x8(bf16x8 v) {
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = (f16)(float)v[i];
+  return r;
+}
 
 // Order-preserving map of an fp32 value to uint32 (larger float -> larger key).
 AS_DEVICE uint32_t f32_key(float f) {
@@ -67,39 +86,39 @@ hipError_t launch_tree_prep(const int32_t *tokens, const int32_t *parents,
                             const int32_t *prefix_len, int B, int n1, int V, int capacity,
                             TreeMeta meta, int32_t *status, hipStream_t s);
 
-template <typename T>
-hipError_t launch_embed(const T *embed, const int32_t *tok, float *x, int rows, int d,
+template <typename TW>
+hipError_t launch_embed(const TW *embed, const int32_t *tok, float *x, int rows, int d,
                         hipStream_t s);
 
-template <typename T>
-hipError_t launch_rmsnorm(const float *x, const T *gain, T *out, int rows, int d, float eps,
-                          hipStream_t s);
+// y = x / sqrt(mean(x^2) + eps) * gain, rounded once to the activation type.
+template <typename TW, typename TIN>
+hipError_t launch_rmsnorm(const TIN *x, const TW *gain, typename ActOf<TW>::type *out, int rows,
+                          int d, float eps, hipStream_t s);
 
-// Same, for inputs already in the model dtype (LM-head tail).
-template <typename T>
-hipError_t launch_rmsnorm_in(const T *x, const T *gain, T *out, int rows, int d, float eps,
-                             hipStream_t s);
-
-template <typename T>
-hipError_t launch_rope_kv(T *qkv, const TreeMeta &meta, T *cache_k, T *cache_v,
-                          int B, int n1, int H, int Hkv, int hd, int capacity,
-                          const double *inv_freq, hipStream_t s);
+// RoPE on q and k of the fp32 QKV projection; q goes to q_out (activation type,
+// [rows, H*hd]), k and v to the cache slots of the tree rows.
+template <typename TW>
+hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
+                          const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
+                          int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s);
 
 enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
 
 // C[M, N] = A[M, K] . W[N, K]^T with the epilogue:
-//  EPI_STORE : out (model dtype) [M, N]
+//  EPI_STORE : out (activation type) [M, N]
 //  EPI_RESID : resid (fp32) [M, N] += C
 //  EPI_SWIGLU: W holds 2F rows (gate, up); out[M, F] = silu(gate) * up, N = F
 //  EPI_F32   : outf (fp32) [M, N] = C
-template <typename T>
-hipError_t launch_gemm(int epi, const T *A, const T *W, int M, int N, int K, T *out,
-                       float *outf, hipStream_t s);
+// TA is the storage type of A (the activation type, or the weight type for a raw input).
+template <typename TW, typename TA>
+hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
+                       typename ActOf<TW>::type *out, float *outf, hipStream_t s);
 
-template <typename T>
-hipError_t launch_attention(const T *qkv, const T *cache_k, const T *cache_v,
-                            const TreeMeta &meta, T *out, float *part_o, float *part_ml,
-                            int part_capacity, int B, int n1, int H, int Hkv, int hd,
+template <typename TW>
+hipError_t launch_attention(const typename ActOf<TW>::type *q, const TW *cache_k,
+                            const TW *cache_v, const TreeMeta &meta,
+                            typename ActOf<TW>::type *out, float *part_o, float *part_ml,
+                            long long part_capacity, int B, int n1, int H, int Hkv, int hd,
                             int capacity, hipStream_t s, int *nsplit_used);
 
 struct VocabArgs {

@@ -1,11 +1,13 @@
 // Embedding gather, RMSNorm, and RoPE with the tree K/V write into the cache.
 //
-// RMSNorm: y = x / sqrt(mean(x^2) + eps) * gain, fp32 math, rounded once to the model
-// dtype.  The residual stream x stays fp32 between layers.
+// RMSNorm: y = x / sqrt(mean(x^2) + eps) * gain, fp32 math, rounded once to the
+// activation type.  The residual stream x stays fp32 between layers.
 // RoPE (rotate-half): the pair (i, i + hd/2) of every query and key head is rotated by
 // pos * base^(-2i/hd); the angle and its sine/cosine are evaluated in double so that
-// large positions (16k-token prefixes) keep full fp32 accuracy.  Tree row r of session
-// b sits at position prefix_len + depth(r) and its key/value go to slot prefix_len + r.
+// large positions (16k-token prefixes) keep full fp32 accuracy.  The QKV projection
+// arrives in fp32 and is rounded once: q to the activation type, k and v to the cache
+// dtype.  Tree row r of session b sits at position prefix_len + depth(r) and its
+// key/value go to slot prefix_len + r.
 #include "common.h"
 
 namespace {
@@ -20,10 +22,10 @@ __global__ void embed_kernel(const T *__restrict__ embed, const int32_t *__restr
 }
 
 // One 256-thread block per row; d is a multiple of 64.
-template <typename Tin, typename T>
+template <typename Tin, typename TG, typename Tout>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const Tin *__restrict__ x,
-                                                      const T *__restrict__ gain,
-                                                      T *__restrict__ out, int d, float eps) {
+                                                      const TG *__restrict__ gain,
+                                                      Tout *__restrict__ out, int d, float eps) {
   const int row = blockIdx.x;
   const Tin *xr = x + (size_t)row * d;
   float ss = 0.f;
@@ -37,16 +39,17 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const Tin *__restrict__ x,
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float scale = 1.0f / sqrtf(tot / (float)d + eps);
-  T *o = out + (size_t)row * d;
+  Tout *o = out + (size_t)row * d;
   for (int i = threadIdx.x; i < d; i += 256)
-    o[i] = from_f32<T>(to_f32(xr[i]) * scale * to_f32(gain[i]));
+    o[i] = from_f32<Tout>(to_f32(xr[i]) * scale * to_f32(gain[i]));
 }
 
 // grid: (rows); block: hd/2 threads (one per rotation pair), looping over heads.
-template <typename T>
-__global__ void rope_kv_kernel(T *__restrict__ qkv, TreeMeta meta, T *__restrict__ ck,
-                               T *__restrict__ cv, int n1, int H, int Hkv, int hd,
-                               int capacity, const double *__restrict__ inv_freq) {
+template <typename TW, typename TA>
+__global__ void rope_kv_kernel(const float *__restrict__ qkv, TA *__restrict__ q_out,
+                               TreeMeta meta, TW *__restrict__ ck, TW *__restrict__ cv, int n1,
+                               int H, int Hkv, int hd, int capacity,
+                               const double *__restrict__ inv_freq) {
   const int row = blockIdx.x;
   const int i = threadIdx.x;  // pair index < hd/2
   const int half = hd >> 1;
@@ -55,23 +58,24 @@ __global__ void rope_kv_kernel(T *__restrict__ qkv, TreeMeta meta, T *__restrict
   double sd, cd;
   sincos(ang, &sd, &cd);
   const float c = (float)cd, s = (float)sd;
-  T *base = qkv + (size_t)row * (H + 2 * Hkv) * hd;
+  const float *base = qkv + (size_t)row * (H + 2 * Hkv) * hd;
+  TA *qo = q_out + (size_t)row * H * hd;
   for (int h = 0; h < H; ++h) {
-    T *q = base + h * hd;
-    const float x1 = to_f32(q[i]), x2 = to_f32(q[i + half]);
-    q[i] = from_f32<T>(x1 * c - x2 * s);
-    q[i + half] = from_f32<T>(x2 * c + x1 * s);
+    const float *q = base + h * hd;
+    const float x1 = q[i], x2 = q[i + half];
+    qo[h * hd + i] = from_f32<TA>(x1 * c - x2 * s);
+    qo[h * hd + i + half] = from_f32<TA>(x2 * c + x1 * s);
   }
   const int slot = meta.sess_S[b] + r;
   for (int g = 0; g < Hkv; ++g) {
-    const T *k = base + (H + g) * hd;
-    const T *v = base + (H + Hkv + g) * hd;
-    const float x1 = to_f32(k[i]), x2 = to_f32(k[i + half]);
+    const float *k = base + (H + g) * hd;
+    const float *v = base + (H + Hkv + g) * hd;
+    const float x1 = k[i], x2 = k[i + half];
     const size_t dst = (((size_t)b * Hkv + g) * capacity + slot) * hd;
-    ck[dst + i] = from_f32<T>(x1 * c - x2 * s);
-    ck[dst + i + half] = from_f32<T>(x2 * c + x1 * s);
-    cv[dst + i] = v[i];
-    cv[dst + i + half] = v[i + half];
+    ck[dst + i] = from_f32<TW>(x1 * c - x2 * s);
+    ck[dst + i + half] = from_f32<TW>(x2 * c + x1 * s);
+    cv[dst + i] = from_f32<TW>(v[i]);
+    cv[dst + i + half] = from_f32<TW>(v[i + half]);
   }
 }
 
@@ -86,42 +90,39 @@ hipError_t launch_embed(const T *embed, const int32_t *tok, float *x, int rows, 
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_rmsnorm(const float *x, const T *gain, T *out, int rows, int d, float eps,
-                          hipStream_t s) {
-  hipLaunchKernelGGL((rmsnorm_kernel<float, T>), dim3(rows), dim3(256), 0, s, x, gain, out, d,
-                     eps);
+template <typename TW, typename TIN>
+hipError_t launch_rmsnorm(const TIN *x, const TW *gain, typename ActOf<TW>::type *out, int rows,
+                          int d, float eps, hipStream_t s) {
+  hipLaunchKernelGGL((rmsnorm_kernel<TIN, TW, typename ActOf<TW>::type>), dim3(rows), dim3(256),
+                     0, s, x, gain, out, d, eps);
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_rmsnorm_in(const T *x, const T *gain, T *out, int rows, int d, float eps,
-                             hipStream_t s) {
-  hipLaunchKernelGGL((rmsnorm_kernel<T, T>), dim3(rows), dim3(256), 0, s, x, gain, out, d,
-                     eps);
+template <typename TW>
+hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
+                          const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
+                          int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s) {
+  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(B * n1), dim3(hd / 2),
+                     0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity,
+                     inv_freq);
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_rope_kv(T *qkv, const TreeMeta &meta, T *cache_k, T *cache_v, int B,
-                          int n1, int H, int Hkv, int hd, int capacity,
-                          const double *inv_freq, hipStream_t s) {
-  hipLaunchKernelGGL(rope_kv_kernel<T>, dim3(B * n1), dim3(hd / 2), 0, s, qkv, meta, cache_k,
-                     cache_v, n1, H, Hkv, hd, capacity, inv_freq);
-  return hipGetLastError();
-}
-
-#define INST(T)                                                                           \
-  template hipError_t launch_embed<T>(const T *, const int32_t *, float *, int, int,       \
-                                      hipStream_t);                                       \
-  template hipError_t launch_rmsnorm<T>(const float *, const T *, T *, int, int, float,    \
-                                        hipStream_t);                                     \
-  template hipError_t launch_rmsnorm_in<T>(const T *, const T *, T *, int, int, float,     \
-                                           hipStream_t);                                  \
-  template hipError_t launch_rope_kv<T>(T *, const TreeMeta &, T *, T *, int, int, int,    \
-                                        int, int, int, const double *, hipStream_t);
-INST(float)
-INST(bf16)
-#undef INST
+template hipError_t launch_embed<float>(const float *, const int32_t *, float *, int, int,
+                                        hipStream_t);
+template hipError_t launch_embed<bf16>(const bf16 *, const int32_t *, float *, int, int,
+                                       hipStream_t);
+template hipError_t launch_rmsnorm<float, float>(const float *, const float *, float *, int, int,
+                                                 float, hipStream_t);
+template hipError_t launch_rmsnorm<bf16, float>(const float *, const bf16 *, f16 *, int, int,
+                                                float, hipStream_t);
+template hipError_t launch_rmsnorm<bf16, bf16>(const bf16 *, const bf16 *, f16 *, int, int,
+                                               float, hipStream_t);
+template hipError_t launch_rope_kv<float>(const float *, float *, const TreeMeta &, float *,
+                                          float *, int, int, int, int, int, int, const double *,
+                                          hipStream_t);
+template hipError_t launch_rope_kv<bf16>(const float *, f16 *, const TreeMeta &, bf16 *, bf16 *,
+                                         int, int, int, int, int, int, const double *,
+                                         hipStream_t);
 
 }  // namespace acespec

@@ -1,6 +1,8 @@
 // Dense contractions of the verify forward pass: C[M, N] = A[M, K] . W[N, K]^T.
 //
-// bf16 path: gfx950 MFMA (v_mfma_f32_16x16x32_bf16), fp32 accumulation.
+// bf16 model: weights are bf16, activations arrive in fp16; both operands are staged
+//   into LDS as fp16 (weights converted exactly while staging) and multiplied with
+//   gfx950's v_mfma_f32_16x16x32_f16 (same rate as the bf16 form), fp32 accumulation.
 //   block tile 128 x 128 x 64, 256 threads = 4 waves in a 2 x 2 grid, each wave owning a
 //   64 x 64 sub-tile (4 x 4 MFMA blocks of 16 x 16).  A and W tiles are staged through
 //   LDS, double buffered, with an XOR swizzle of the 16-byte chunks inside each 128-byte
@@ -11,9 +13,9 @@
 //   panel in one L2.
 // fp32 path (small models only): LDS-tiled FMA kernel with the same epilogues.
 //
-// Epilogues fuse the elementwise work that follows each product: bf16 store (QKV),
+// Epilogues fuse the elementwise work that follows each product: fp32 store (QKV, LM head),
 // fp32 residual add (attention output and MLP down projections), SwiGLU (gate/up
-// projection: each tile holds matching gate and up columns), fp32 store (LM head).
+// projection: each tile holds matching gate and up columns), activation-type store.
 #include "common.h"
 
 namespace {
@@ -32,12 +34,20 @@ AS_DEVICE int xcd_tile(int bid, int total) {
   return before + local;
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
-    const bf16 *__restrict__ A, const bf16 *__restrict__ W, int M, int N, int K,
-    bf16 *__restrict__ out, float *__restrict__ outf, int mt, int nt) {
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
+AS_DEVICE f16x8 to_f16x8(f16x8 v) { return v; }
+AS_DEVICE f16x8 to_f16x8(bf16x8 v) { return bf16x8_to_f16x8(v); }
+
+template <typename TA> struct Vec8;
+template <> struct Vec8<f16> { typedef f16x8 type; };
+template <> struct Vec8<bf16> { typedef bf16x8 type; };
+
+template <int EPI, typename TA>
+__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(
+    const TA *__restrict__ A, const bf16 *__restrict__ W, int M, int N, int K,
+    f16 *__restrict__ out, float *__restrict__ outf, int mt, int nt) {
+  typedef typename Vec8<TA>::type va_t;
+  __shared__ __attribute__((aligned(16))) f16 sA[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) f16 sB[2][BN * BK];
 
   const int tile = xcd_tile(blockIdx.x, mt * nt);
   const int tn = tile / mt, tm = tile - tn * mt;
@@ -46,7 +56,8 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
   const int wm = wave >> 1, wn = wave & 1;
 
   // Global source rows of the 4 chunks this thread stages per operand.
-  const bf16 *ga[4], *gb[4];
+  const TA *ga[4];
+  const bf16 *gb[4];
   int lds_off[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -72,16 +83,17 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  bf16x8 ra[4], rb[4];
+  va_t ra[4];
+  bf16x8 rb[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    ra[i] = *(const bf16x8 *)(ga[i]);
+    ra[i] = *(const va_t *)(ga[i]);
     rb[i] = *(const bf16x8 *)(gb[i]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    *(bf16x8 *)(&sA[0][lds_off[i]]) = ra[i];
-    *(bf16x8 *)(&sB[0][lds_off[i]]) = rb[i];
+    *(f16x8 *)(&sA[0][lds_off[i]]) = to_f16x8(ra[i]);
+    *(f16x8 *)(&sB[0][lds_off[i]]) = to_f16x8(rb[i]);
   }
   __syncthreads();
 
@@ -106,28 +118,28 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
       const int koff = (kt + 1) * BK;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        ra[i] = *(const bf16x8 *)(ga[i] + koff);
+        ra[i] = *(const va_t *)(ga[i] + koff);
         rb[i] = *(const bf16x8 *)(gb[i] + koff);
       }
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      bf16x8 fa[4], fb[4];
+      f16x8 fa[4], fb[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = *(const bf16x8 *)(&sA[cur][swz(arow[i], s * 4 + lk)]);
+      for (int i = 0; i < 4; ++i) fa[i] = *(const f16x8 *)(&sA[cur][swz(arow[i], s * 4 + lk)]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = *(const bf16x8 *)(&sB[cur][swz(brow[j], s * 4 + lk)]);
+      for (int j = 0; j < 4; ++j) fb[j] = *(const f16x8 *)(&sB[cur][swz(brow[j], s * 4 + lk)]);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
     }
     if (more) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        *(bf16x8 *)(&sA[cur ^ 1][lds_off[i]]) = ra[i];
-        *(bf16x8 *)(&sB[cur ^ 1][lds_off[i]]) = rb[i];
+        *(f16x8 *)(&sA[cur ^ 1][lds_off[i]]) = to_f16x8(ra[i]);
+        *(f16x8 *)(&sB[cur ^ 1][lds_off[i]]) = to_f16x8(rb[i]);
       }
     }
     __syncthreads();
@@ -144,7 +156,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
 #pragma unroll
         for (int jj = 0; jj < 2; ++jj) {
           const int col = tn * 64 + wn * 32 + jj * 16 + lr;
-          out[(size_t)row * N + col] = (bf16)silu_mul(acc[i][jj][e], acc[i][jj + 2][e]);
+          out[(size_t)row * N + col] = (f16)silu_mul(acc[i][jj][e], acc[i][jj + 2][e]);
         }
       } else {
 #pragma unroll
@@ -152,7 +164,7 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(
           const int col = tn * BN + wn * 64 + j * 16 + lr;
           if (col >= N) continue;
           const size_t o = (size_t)row * N + col;
-          if (EPI == acespec::EPI_STORE) out[o] = (bf16)acc[i][j][e];
+          if (EPI == acespec::EPI_STORE) out[o] = (f16)acc[i][j][e];
           else if (EPI == acespec::EPI_RESID) outf[o] += acc[i][j][e];
           else outf[o] = acc[i][j][e];
         }
@@ -239,35 +251,47 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
 
 namespace acespec {
 
-template <>
-hipError_t launch_gemm<bf16>(int epi, const bf16 *A, const bf16 *W, int M, int N, int K,
-                             bf16 *out, float *outf, hipStream_t s) {
+template <typename TA>
+hipError_t launch_mfma(int epi, const TA *A, const bf16 *W, int M, int N, int K, f16 *out,
+                       float *outf, hipStream_t s) {
   const int mt = (M + BM - 1) / BM;
   const int nt = epi == EPI_SWIGLU ? N / 64 : (N + BN - 1) / BN;
   const dim3 grid(mt * nt), block(256);
   switch (epi) {
     case EPI_STORE:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, grid, block, 0, s, A, W, M, N, K, out,
-                         outf, mt, nt);
+      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_STORE, TA>), grid, block, 0, s, A, W, M, N, K,
+                         out, outf, mt, nt);
       break;
     case EPI_RESID:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_RESID>, grid, block, 0, s, A, W, M, N, K, out,
-                         outf, mt, nt);
+      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_RESID, TA>), grid, block, 0, s, A, W, M, N, K,
+                         out, outf, mt, nt);
       break;
     case EPI_SWIGLU:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, block, 0, s, A, W, M, N, K, out,
-                         outf, mt, nt);
+      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_SWIGLU, TA>), grid, block, 0, s, A, W, M, N, K,
+                         out, outf, mt, nt);
       break;
     default:
-      hipLaunchKernelGGL(gemm_bf16_kernel<EPI_F32>, grid, block, 0, s, A, W, M, N, K, out,
-                         outf, mt, nt);
+      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_F32, TA>), grid, block, 0, s, A, W, M, N, K,
+                         out, outf, mt, nt);
   }
   return hipGetLastError();
 }
 
 template <>
-hipError_t launch_gemm<float>(int epi, const float *A, const float *W, int M, int N, int K,
-                              float *out, float *outf, hipStream_t s) {
+hipError_t launch_gemm<bf16, f16>(int epi, const f16 *A, const bf16 *W, int M, int N, int K,
+                                  f16 *out, float *outf, hipStream_t s) {
+  return launch_mfma<f16>(epi, A, W, M, N, K, out, outf, s);
+}
+
+template <>
+hipError_t launch_gemm<bf16, bf16>(int epi, const bf16 *A, const bf16 *W, int M, int N, int K,
+                                   f16 *out, float *outf, hipStream_t s) {
+  return launch_mfma<bf16>(epi, A, W, M, N, K, out, outf, s);
+}
+
+template <>
+hipError_t launch_gemm<float, float>(int epi, const float *A, const float *W, int M, int N,
+                                     int K, float *out, float *outf, hipStream_t s) {
   const dim3 grid((N + 63) / 64, (M + 63) / 64), block(256);
   switch (epi) {
     case EPI_STORE:
