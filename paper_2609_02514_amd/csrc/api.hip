@@ -54,6 +54,9 @@ struct acespec_ctx {
   void *a = nullptr, *attn = nullptr, *q = nullptr, *h = nullptr;  // activation type
   float *qkv = nullptr;                                              // fp32 projection
   long long part_cap = 0;
+  float *gpart = nullptr;     // split-K partials of the GEMMs
+  long long gpart_cap = 0;
+  int cus = 256;
   double *inv_freq = nullptr;
   TreeMeta meta{};
   // timing
@@ -136,6 +139,7 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   const int F = d.d_ff, V = d.vocab, QKVN = (H + 2 * Hkv) * hd;
   const int cap = kv->capacity;
   A *x_a = (A *)ctx->a, *x_attn = (A *)ctx->attn, *x_q = (A *)ctx->q, *x_h = (A *)ctx->h;
+  const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus};
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
   const TreeMeta &meta = ctx->meta;
 
@@ -150,25 +154,25 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
     RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.attn_norm, x_a, R, D,
                                              d.rms_eps, stream)));
     RUN(K_GEMM_QKV, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)lw.wqkv, R, QKVN, D, nullptr,
-                                       ctx->qkv, stream)));
+                                       ctx->qkv, aux, stream)));
     RUN(K_ROPE, launch_rope_kv<T>(ctx->qkv, x_q, meta, ck, cv, B, n1, H, Hkv, hd, cap,
                                   ctx->inv_freq, stream));
     int nsplit = 1;
     RUN(K_ATTN, launch_attention<T>(x_q, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
                                     ctx->part_cap, B, n1, H, Hkv, hd, cap, stream, &nsplit));
     RUN(K_GEMM_O, (launch_gemm<T, A>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
-                                     ctx->x, stream)));
+                                     ctx->x, aux, stream)));
     RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D,
                                              d.rms_eps, stream)));
     RUN(K_GEMM_GATE_UP, (launch_gemm<T, A>(EPI_SWIGLU, x_a, (const T *)lw.w_gate_up, R, F, D,
-                                           x_h, nullptr, stream)));
+                                           x_h, nullptr, aux, stream)));
     RUN(K_GEMM_DOWN, (launch_gemm<T, A>(EPI_RESID, x_h, (const T *)lw.w_down, R, D, F, nullptr,
-                                        ctx->x, stream)));
+                                        ctx->x, aux, stream)));
   }
   RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)w->final_norm, x_a, R, D,
                                            d.rms_eps, stream)));
   RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr,
-                                    logits, stream)));
+                                    logits, aux, stream)));
   VocabArgs va;
   va.logits = logits;
   va.q = draft_q;
@@ -203,14 +207,20 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   const acespec_model_desc &d = ctx->d;
   const int D = d.d_model, V = d.vocab;
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
+  const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus};
   if (final_norm) {
     RUN(K_RMSNORM, (launch_rmsnorm<T, T>((const T *)hidden, (const T *)final_norm, (A *)ctx->a,
                                          R, D, d.rms_eps, stream)));
     RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)ctx->a, (const T *)lm_head, R, V, D,
-                                      nullptr, logits, stream)));
+                                      nullptr, logits, aux, stream)));
+  } else if (sizeof(T) == 2) {  // bf16 hidden states: widen to fp16 for the f16 MFMA path
+    RUN(K_RMSNORM, launch_cast_bf16_f16((const bf16 *)hidden, (f16 *)ctx->a, (size_t)R * D,
+                                        stream));
+    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)ctx->a, (const T *)lm_head, R, V, D,
+                                      nullptr, logits, aux, stream)));
   } else {
-    RUN(K_GEMM_LM, (launch_gemm<T, T>(EPI_F32, (const T *)hidden, (const T *)lm_head, R, V, D,
-                                      nullptr, logits, stream)));
+    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)hidden, (const T *)lm_head, R, V, D,
+                                      nullptr, logits, aux, stream)));
   }
   VocabArgs va;
   va.logits = logits;
@@ -285,7 +295,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
-  void *p_qkv = nullptr;
+  void *p_qkv = nullptr, *p_gpart = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
@@ -299,6 +309,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       {(size_t)c->part_cap * 4, &p_po},
       {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
       {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
+      {(size_t)8 * R * d.d_model * 4, &p_gpart},
       {R * 4, &p_tok}, {R * 4, &p_par}, {R * 4, &p_pos}, {R * 4, &p_depth}, {R * 8, &p_anc},
       {(size_t)max_batch * 4, &p_S}};
   size_t total = 0;
@@ -315,6 +326,14 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   }
   c->x = (float *)p_x;
   c->qkv = (float *)p_qkv;
+  c->gpart = (float *)p_gpart;
+  c->gpart_cap = (long long)8 * R * d.d_model;
+  {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+      c->cus = n;
+  }
   c->logits = (float *)p_logits;
   c->part_o = (float *)p_po;
   c->part_ml = (float *)p_pml;

@@ -109,10 +109,26 @@ enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
 //  EPI_RESID : resid (fp32) [M, N] += C
 //  EPI_SWIGLU: W holds 2F rows (gate, up); out[M, F] = silu(gate) * up, N = F
 //  EPI_F32   : outf (fp32) [M, N] = C
-// TA is the storage type of A (the activation type, or the weight type for a raw input).
+// A is in the activation type.  aux.part: fp32 workspace for split-K partials
+// (aux.part_cap floats), aux.cus: compute units of the device.
+struct GemmAux {
+  float *part;
+  long long part_cap;
+  int cus;
+};
 template <typename TW, typename TA>
 hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
-                       typename ActOf<TW>::type *out, float *outf, hipStream_t s);
+                       typename ActOf<TW>::type *out, float *outf, const GemmAux &aux,
+                       hipStream_t s);
+
+// The fp16 x bf16 GEMM with an explicit tiling (var >= 0) and split count
+// (splits_override > 0); var < 0 / splits_override <= 0 choose automatically.
+hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
+                               const bf16 *W, int M, int N, int K, f16 *out, float *outf,
+                               float *part, long long part_cap, int cus, hipStream_t s);
+
+// Exact widening of a bf16 tensor to fp16 (in range), n elements.
+hipError_t launch_cast_bf16_f16(const bf16 *in, f16 *out, size_t n, hipStream_t s);
 
 template <typename TW>
 hipError_t launch_attention(const typename ActOf<TW>::type *q, const TW *cache_k,

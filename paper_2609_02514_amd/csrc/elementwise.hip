@@ -79,9 +79,22 @@ __global__ void rope_kv_kernel(const float *__restrict__ qkv, TA *__restrict__ q
   }
 }
 
+__global__ void cast_bf16_f16_kernel(const bf16x8 *__restrict__ in, f16x8 *__restrict__ out,
+                                     size_t n8) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n8) out[i] = bf16x8_to_f16x8(in[i]);
+}
+
 }  // namespace
 
 namespace acespec {
+
+hipError_t launch_cast_bf16_f16(const bf16 *in, f16 *out, size_t n, hipStream_t s) {
+  const size_t n8 = n / 8;  // n is a multiple of 64 (rows x d_model)
+  hipLaunchKernelGGL(cast_bf16_f16_kernel, dim3((n8 + 255) / 256), dim3(256), 0, s,
+                     (const bf16x8 *)in, (f16x8 *)out, n8);
+  return hipGetLastError();
+}
 
 template <typename T>
 hipError_t launch_embed(const T *embed, const int32_t *tok, float *x, int rows, int d,

@@ -1,28 +1,24 @@
 // Dense contractions of the verify forward pass: C[M, N] = A[M, K] . W[N, K]^T.
 //
 // bf16 model: weights are bf16, activations arrive in fp16; both operands are staged
-//   into LDS as fp16 (weights converted exactly while staging) and multiplied with
-//   gfx950's v_mfma_f32_16x16x32_f16 (same rate as the bf16 form), fp32 accumulation.
-//   block tile 128 x 128 x 64, 256 threads = 4 waves in a 2 x 2 grid, each wave owning a
-//   64 x 64 sub-tile (4 x 4 MFMA blocks of 16 x 16).  A and W tiles are staged through
-//   LDS, double buffered, with an XOR swizzle of the 16-byte chunks inside each 128-byte
-//   row so that both the stores and the per-lane 16-byte fragment reads are free of
-//   bank conflicts.  The next tile's global loads are in flight while the current tile
-//   is multiplied.  Tiles are ordered so that the row tiles of one weight panel land on
-//   the same XCD (workgroups are dealt round-robin over the 8 XCDs), which keeps that
-//   panel in one L2.
-// fp32 path (small models only): LDS-tiled FMA kernel with the same epilogues.
+//   into LDS and the weight fragments are converted to fp16 (exactly) as they are read,
+//   then multiplied with gfx950's v_mfma_f32_16x16x32_f16 (same rate as the bf16 form),
+//   fp32 accumulation.  See the kernel comment below for the tiling and pipeline; tiles
+//   are ordered so that the row tiles of one weight panel land on the same XCD
+//   (workgroups are dealt round-robin over the 8 XCDs), which keeps that panel in one
+//   L2.  GEMMs whose tile count cannot fill the chip split K; the fp32 partials are
+//   summed in a fixed order (deterministic) by a small reduction kernel.
+// fp32 model (small models only): LDS-tiled FMA kernel with the same epilogues.
 //
-// Epilogues fuse the elementwise work that follows each product: fp32 store (QKV, LM head),
-// fp32 residual add (attention output and MLP down projections), SwiGLU (gate/up
-// projection: each tile holds matching gate and up columns), activation-type store.
+// Epilogues fuse the elementwise work that follows each product: fp32 store (QKV, LM
+// head), fp32 residual add (attention output and MLP down projections), SwiGLU
+// (gate/up projection: each tile holds matching gate and up columns), activation-type
+// store.
+#include <cmath>
+
 #include "common.h"
 
 namespace {
-
-constexpr int BM = 128, BN = 128, BK = 64;
-
-AS_DEVICE int swz(int row, int chunk) { return row * BK + (((chunk ^ (row & 7))) << 3); }
 
 AS_DEVICE float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
@@ -34,143 +30,217 @@ AS_DEVICE int xcd_tile(int bid, int total) {
   return before + local;
 }
 
-AS_DEVICE f16x8 to_f16x8(f16x8 v) { return v; }
-AS_DEVICE f16x8 to_f16x8(bf16x8 v) { return bf16x8_to_f16x8(v); }
+// ------------------------------------------------------------------------------------
+// fp16 x bf16 MFMA kernel, templated on the tiling.
+//   WMN x WNN waves; each owns a (WTM*16) x (WTN*16) output sub-tile made of 16 x 16 MFMA
+//   blocks, fp32 accumulators in AGPRs.  Block tile TBM x TBN, k-step 32 (64-byte rows).
+//   Operands move HBM -> LDS with gfx950's direct loads (global_load_lds_dwordx4: 64
+//   lanes x 16 bytes land contiguously at a wave-uniform LDS address) through a ring of
+//   NST stages, NST - 2 of them in flight.  The four 16-byte chunks of each 64-byte row
+//   are XOR-swizzled by ((row >> 1) & 3) so that the 16-byte fragment reads of 8
+//   consecutive rows hit 32 distinct banks; since the DMA fixes where each lane's bytes
+//   land, the swizzle is applied to the global source address.
+//   One barrier per stage, placed mid-stage: it certifies that the NEXT stage has landed
+//   for every wave and that the stage loaded NST - 1 ahead is free, so each wave reads
+//   the next stage's first fragments while its last MFMAs of the current stage run.  The
+//   loop body is branch-free (past the end of K the last k-tile is loaded again into a
+//   free stage; next-stage fragments are always read) so the compiler counts
+//   outstanding LDS reads exactly, and fragment reads are fenced against the MFMAs.
+// ------------------------------------------------------------------------------------
+constexpr int KS = 32;  // k per stage
 
-template <typename TA> struct Vec8;
-template <> struct Vec8<f16> { typedef f16x8 type; };
-template <> struct Vec8<bf16> { typedef bf16x8 type; };
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
-template <int EPI, typename TA>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(
-    const TA *__restrict__ A, const bf16 *__restrict__ W, int M, int N, int K,
-    f16 *__restrict__ out, float *__restrict__ outf, int mt, int nt) {
-  typedef typename Vec8<TA>::type va_t;
-  __shared__ __attribute__((aligned(16))) f16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) f16 sB[2][BN * BK];
+AS_DEVICE void dma16(const void *g, lds_ptr_t l) {
+  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+}
+// 64-byte rows, 16-byte chunks swizzled by (row >> 1) & 3; returns an element offset.
+AS_DEVICE int swz32(int row, int chunk) { return row * KS + ((chunk ^ ((row >> 1) & 3)) << 3); }
 
-  const int tile = xcd_tile(blockIdx.x, mt * nt);
-  const int tn = tile / mt, tm = tile - tn * mt;
-  const int m0 = tm * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+template <int VM> AS_DEVICE void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
-  // Global source rows of the 4 chunks this thread stages per operand.
-  const TA *ga[4];
-  const bf16 *gb[4];
-  int lds_off[4];
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+template <int EPI, int WMN, int WNN, int WTM, int WTN, int NST, int OCC>
+__global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
+    const f16 *__restrict__ A, const bf16 *__restrict__ W, int M, int N, int K,
+    f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
+    int splits) {
+  constexpr int NW = WMN * WNN;
+  constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
+  constexpr int A_BYTES = TBM * KS * 2, B_BYTES = TBN * KS * 2;
+  constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  constexpr int A_DMA = A_BYTES / 1024 / NW, B_DMA = B_BYTES / 1024 / NW;
+  constexpr int L_DMA = A_DMA + B_DMA;
+  static_assert(A_DMA * 1024 * NW == A_BYTES && B_DMA * 1024 * NW == B_BYTES, "DMA split");
+  static_assert(WTM >= 4 && NST >= 3, "pipeline shape");
+  constexpr int HALF = WTN / 2;  // SwiGLU: gate blocks, then the matching up blocks
+  __shared__ __attribute__((aligned(16))) char smem[NST * STAGE_BYTES];
+
+  const int units = mt * nt * splits;
+  const int unit = xcd_tile(blockIdx.x, units);
+  const int tn = unit / (mt * splits);
+  const int rem = unit - tn * (mt * splits);
+  const int tm = rem / splits, sp = rem - tm * splits;
+  const int m0 = tm * TBM;
+  const int KT = K / KS;
+  const int kt0 = (int)((long long)KT * sp / splits), kt1 = (int)((long long)KT * (sp + 1) / splits);
+  const int nk = kt1 - kt0;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w / WNN, wn = w - wm * WNN;
+  const int lr = lane & 15, lk = lane >> 4;
+
+  // DMA sources: block j covers tile rows 16j..16j+15; lane l lands at row 16j + l/4,
+  // physical chunk l%4, which holds logical chunk (l%4) ^ ((row >> 1) & 3).
+  const int drow = lane >> 2, dchunk = (lane & 3) ^ ((lane >> 3) & 3);
+  const f16 *ga[A_DMA];
+  const bf16 *gb[B_DMA];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-    int am = m0 + row;
-    am = am < M ? am : M - 1;
-    ga[i] = A + (size_t)am * K + kc * 8;
+  for (int t = 0; t < A_DMA; ++t) {
+    int r = m0 + (w * A_DMA + t) * 16 + drow;
+    r = r < M ? r : M - 1;
+    ga[t] = A + (size_t)r * K + dchunk * 8;
+  }
+#pragma unroll
+  for (int t = 0; t < B_DMA; ++t) {
+    const int row = (w * B_DMA + t) * 16 + drow;  // W-tile row
     int wr;
     if (EPI == acespec::EPI_SWIGLU) {
-      const int j0 = tn * 64;  // N is the SwiGLU output width F here
-      wr = row < 64 ? j0 + row : N + j0 + (row - 64);
+      const int j = tn * (TBN / 2) + (row % (TBN / 2));
+      const int jc = j < N ? j : N - 1;
+      wr = row < TBN / 2 ? jc : N + jc;
     } else {
-      wr = tn * BN + row;
+      wr = tn * TBN + row;
       wr = wr < N ? wr : N - 1;
     }
-    gb[i] = W + (size_t)wr * K + kc * 8;
-    lds_off[i] = swz(row, kc);
+    gb[t] = W + (size_t)wr * K + dchunk * 8;
+  }
+  auto issue = [&](int kt, int stage) {
+    char *base = smem + stage * STAGE_BYTES;
+    const int koff = kt * KS;
+#pragma unroll
+    for (int t = 0; t < A_DMA; ++t)
+      dma16(ga[t] + koff, (lds_ptr_t)(base + (w * A_DMA + t) * 1024));
+#pragma unroll
+    for (int t = 0; t < B_DMA; ++t)
+      dma16(gb[t] + koff, (lds_ptr_t)(base + A_BYTES + (w * B_DMA + t) * 1024));
+  };
+
+  int boff[WTN], aoff[WTM];
+#pragma unroll
+  for (int j = 0; j < WTN; ++j) {
+    const int brow = (EPI == acespec::EPI_SWIGLU)
+                         ? (j < HALF ? wn * HALF * 16 + j * 16
+                                     : TBN / 2 + wn * HALF * 16 + (j - HALF) * 16) + lr
+                         : wn * WTN * 16 + j * 16 + lr;
+    boff[j] = swz32(brow, lk);
+  }
+#pragma unroll
+  for (int ii = 0; ii < WTM; ++ii) aoff[ii] = swz32(wm * WTM * 16 + ii * 16 + lr, lk);
+
+  f32x4 acc[WTM][WTN];
+#pragma unroll
+  for (int i = 0; i < WTM; ++i)
+#pragma unroll
+    for (int j = 0; j < WTN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int p = 0; p < NST - 1; ++p) issue(kt0 + (p < nk ? p : nk - 1), p);
+  wait_vmcnt<(NST - 2) * L_DMA>();  // stage 0 landed for this wave
+  __builtin_amdgcn_s_barrier();
+  f16x8 fb[WTN], fa[WTM];
+  bf16x8 rbn[WTN];
+  {
+    const bf16 *sB = (const bf16 *)(smem + A_BYTES);
+    const f16 *sA = (const f16 *)smem;
+#pragma unroll
+    for (int j = 0; j < WTN; ++j) fb[j] = bf16x8_to_f16x8(*(const bf16x8 *)(&sB[boff[j]]));
+    fa[0] = *(const f16x8 *)(&sA[aoff[0]]);
+    fa[1] = *(const f16x8 *)(&sA[aoff[1]]);
   }
 
-  f32x4 acc[4][4];
+  for (int i = 0; i < nk; ++i) {
+    const int cur = i % NST, nxt = (i + 1) % NST;
+    const f16 *sA = (const f16 *)(smem + cur * STAGE_BYTES);
+    const f16 *sAn = (const f16 *)(smem + nxt * STAGE_BYTES);
+    const bf16 *sBn = (const bf16 *)(smem + nxt * STAGE_BYTES + A_BYTES);
+    const int knext = i + NST - 1 < nk ? i + NST - 1 : nk - 1;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int ii = 0; ii < WTM; ++ii) {
+      if (ii + 2 < WTM) fa[ii + 2] = *(const f16x8 *)(&sA[aoff[ii + 2]]);
+      if (ii == WTM / 2) {
+        // stage i+1 has landed for this wave (NST-3 newer stages may be outstanding);
+        // after the barrier it has landed for every wave and stage i-1 is free
+        wait_vmcnt<(NST - 3) * L_DMA>();
+        __builtin_amdgcn_s_barrier();
+        issue(kt0 + knext, (i + NST - 1) % NST);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  va_t ra[4];
-  bf16x8 rb[4];
+        for (int j = 0; j < WTN; ++j) rbn[j] = *(const bf16x8 *)(&sBn[boff[j]]);
+      }
+      SCHED_FENCE();
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = *(const va_t *)(ga[i]);
-    rb[i] = *(const bf16x8 *)(gb[i]);
-  }
+      for (int j = 0; j < WTN; ++j)
+        acc[ii][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[ii], fb[j], acc[ii][j], 0, 0, 0);
+      SCHED_FENCE();
+      if (ii == WTM - 2) fa[0] = *(const f16x8 *)(&sAn[aoff[0]]);
+      if (ii == WTM - 1) {
+        fa[1] = *(const f16x8 *)(&sAn[aoff[1]]);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    *(f16x8 *)(&sA[0][lds_off[i]]) = to_f16x8(ra[i]);
-    *(f16x8 *)(&sB[0][lds_off[i]]) = to_f16x8(rb[i]);
-  }
-  __syncthreads();
-
-  // Fragment rows for this lane.
-  const int lr = lane & 15, lk = lane >> 4;
-  int arow[4], brow[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) arow[i] = wm * 64 + i * 16 + lr;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (EPI == acespec::EPI_SWIGLU)
-      brow[j] = (j < 2 ? wn * 32 + j * 16 : 64 + wn * 32 + (j - 2) * 16) + lr;
-    else
-      brow[j] = wn * 64 + j * 16 + lr;
-  }
-
-  const int KT = K / BK;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) {
-      const int koff = (kt + 1) * BK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = *(const va_t *)(ga[i] + koff);
-        rb[i] = *(const bf16x8 *)(gb[i] + koff);
+        for (int j = 0; j < WTN; ++j) fb[j] = bf16x8_to_f16x8(rbn[j]);
       }
     }
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f16x8 fa[4], fb[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = *(const f16x8 *)(&sA[cur][swz(arow[i], s * 4 + lk)]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) fb[j] = *(const f16x8 *)(&sB[cur][swz(brow[j], s * 4 + lk)]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *(f16x8 *)(&sA[cur ^ 1][lds_off[i]]) = to_f16x8(ra[i]);
-        *(f16x8 *)(&sB[cur ^ 1][lds_off[i]]) = to_f16x8(rb[i]);
-      }
-    }
-    __syncthreads();
   }
+  // No LDS DMA may still be writing when the workgroup's LDS is released.
+  wait_vmcnt<0>();
 
-  // Epilogue.  acc[i][j][e] is C[row = .. + lk*4 + e][col = .. + lr].
+  // Epilogue.  acc[i][j][e] is C[row = m0 + wm*WTM*16 + i*16 + lk*4 + e][col = .. + lr].
+  const size_t MN = (size_t)M * N;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int ii = 0; ii < WTM; ++ii) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int row = m0 + wm * 64 + i * 16 + lk * 4 + e;
+      const int row = m0 + wm * WTM * 16 + ii * 16 + lk * 4 + e;
       if (row >= M) continue;
       if (EPI == acespec::EPI_SWIGLU) {
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int col = tn * 64 + wn * 32 + jj * 16 + lr;
-          out[(size_t)row * N + col] = (f16)silu_mul(acc[i][jj][e], acc[i][jj + 2][e]);
+        for (int jj = 0; jj < HALF; ++jj) {
+          const int col = tn * (TBN / 2) + wn * HALF * 16 + jj * 16 + lr;
+          if (col < N)
+            out[(size_t)row * N + col] = (f16)silu_mul(acc[ii][jj][e], acc[ii][jj + HALF][e]);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int col = tn * BN + wn * 64 + j * 16 + lr;
+        for (int j = 0; j < WTN; ++j) {
+          const int col = tn * TBN + wn * WTN * 16 + j * 16 + lr;
           if (col >= N) continue;
           const size_t o = (size_t)row * N + col;
-          if (EPI == acespec::EPI_STORE) out[o] = (f16)acc[i][j][e];
-          else if (EPI == acespec::EPI_RESID) outf[o] += acc[i][j][e];
-          else outf[o] = acc[i][j][e];
+          if (splits > 1) part[sp * MN + o] = acc[ii][j][e];
+          else if (EPI == acespec::EPI_STORE) out[o] = (f16)acc[ii][j][e];
+          else if (EPI == acespec::EPI_RESID) outf[o] += acc[ii][j][e];
+          else outf[o] = acc[ii][j][e];
         }
       }
     }
   }
+}
+
+// Split-K reduction in a fixed order (deterministic): dst (+)= sum_s part[s].
+template <bool RESID>
+__global__ void splitk_reduce_kernel(const float4 *__restrict__ part, float4 *__restrict__ dst,
+                                     size_t n4, int splits) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  float4 acc = RESID ? dst[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s = 0; s < splits; ++s) {
+    const float4 v = part[s * n4 + i];
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  dst[i] = acc;
 }
 
 // ------------------------------------------------------------------------------------
@@ -247,51 +317,117 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
   }
 }
 
+using acespec::EPI_STORE;
+using acespec::EPI_RESID;
+using acespec::EPI_SWIGLU;
+using acespec::EPI_F32;
+
+// Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU}.
+// Measured on MI355X against the verify-step shapes (other tilings tried: 32 x 32 MFMA
+// blocks with one wave per SIMD, 64-wide k stages, weights loaded straight to VGPRs,
+// deeper rings at one workgroup per CU; none was faster than these two).
+struct GemmVariant {
+  int wmn, wnn, wtm, wtn, nst, occ;
+};
+constexpr GemmVariant kVariants[] = {
+    {1, 4, 8, 4, 3, 2},  // 0: 128 x 256, wave 128 x 64, 72 KB LDS, 2 workgroups per CU
+    {2, 2, 4, 4, 4, 2},  // 1: 128 x 128, wave 64 x 64, 64 KB LDS, 2 workgroups per CU
+};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+
+// Chooses the number of K splits: enough units to fill the chip, weighed against the
+// cost of re-reading fp32 partials.  Only residual / fp32 epilogues split.
+int choose_splits(int epi, int M, int N, int K, int tiles, int cus, int occ) {
+  if (epi == EPI_SWIGLU || epi == EPI_STORE || (N % 4) != 0) return 1;
+  const int KT = K / 64;
+  const double part_cost = (double)M * N * 4 / 10e12 / 0.43e-6;  // per split, in 64-k units
+  int best = 1;
+  double best_t = 1e30;
+  for (int s = 1; s <= 8; ++s) {
+    if (KT / s < 4) break;
+    const double rounds = std::ceil((double)tiles * s / ((double)cus * occ));
+    const double t = rounds * std::ceil((double)KT / s) + (s > 1 ? part_cost * s : 0.0);
+    if (t < best_t * 0.97) { best_t = t; best = s; }
+  }
+  return best;
+}
+
+template <int EPI, int V>
+void launch_variant(dim3 grid, hipStream_t s, const f16 *A, const bf16 *W, int M, int N, int K,
+                    f16 *out, float *outf, float *part, int mt, int nt, int splits) {
+  constexpr GemmVariant v = kVariants[V];
+  hipLaunchKernelGGL((gemm_f16w_kernel<EPI, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ>), grid,
+                     dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
+                     splits);
+}
+
+template <int EPI>
+void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const bf16 *W, int M, int N,
+                int K, f16 *out, float *outf, float *part, int mt, int nt, int splits) {
+  switch (var) {
+#define CASE(V) case V: launch_variant<EPI, V>(grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    CASE(0) CASE(1)
+#undef CASE
+    default: break;
+  }
+}
+
+// Default tiling per shape (measured on MI355X): 128 x 128 tiles for few rows (more
+// tiles to spread over 256 CUs) and for QKV-sized fp32 outputs, 128 x 256 otherwise.
+int pick_variant(int epi, int M, int N, int K) {
+  (void)K;
+  if (M <= 384) return 1;
+  if (epi == EPI_F32 && N <= 8192) return 1;
+  return 0;
+}
+
 }  // namespace
 
 namespace acespec {
 
-template <typename TA>
-hipError_t launch_mfma(int epi, const TA *A, const bf16 *W, int M, int N, int K, f16 *out,
-                       float *outf, hipStream_t s) {
-  const int mt = (M + BM - 1) / BM;
-  const int nt = epi == EPI_SWIGLU ? N / 64 : (N + BN - 1) / BN;
-  const dim3 grid(mt * nt), block(256);
+hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
+                               const bf16 *W, int M, int N, int K, f16 *out, float *outf,
+                               float *part, long long part_cap, int cus, hipStream_t s) {
+  if (var < 0) var = pick_variant(epi, M, N, K);
+  if (var >= kNumVariants) return hipErrorInvalidValue;
+  const GemmVariant v = kVariants[var];
+  const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
+  const int mt = (M + tbm - 1) / tbm;
+  const int nt = epi == EPI_SWIGLU ? (N + tbn / 2 - 1) / (tbn / 2) : (N + tbn - 1) / tbn;
+  int splits = splits_override > 0 ? splits_override
+                                   : choose_splits(epi, M, N, K, mt * nt, cus, v.occ);
+  if (epi == EPI_SWIGLU || epi == EPI_STORE || (N % 4) != 0) splits = 1;
+  while (splits > 1 && (long long)splits * M * N > part_cap) --splits;
+  const dim3 grid(mt * nt * splits);
   switch (epi) {
-    case EPI_STORE:
-      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_STORE, TA>), grid, block, 0, s, A, W, M, N, K,
-                         out, outf, mt, nt);
-      break;
-    case EPI_RESID:
-      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_RESID, TA>), grid, block, 0, s, A, W, M, N, K,
-                         out, outf, mt, nt);
-      break;
-    case EPI_SWIGLU:
-      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_SWIGLU, TA>), grid, block, 0, s, A, W, M, N, K,
-                         out, outf, mt, nt);
-      break;
-    default:
-      hipLaunchKernelGGL((gemm_mfma_kernel<EPI_F32, TA>), grid, block, 0, s, A, W, M, N, K,
-                         out, outf, mt, nt);
+    case EPI_STORE: launch_epi<EPI_STORE>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    case EPI_RESID: launch_epi<EPI_RESID>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    default: launch_epi<EPI_F32>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const size_t n4 = (size_t)M * N / 4;
+  if (epi == EPI_RESID)
+    hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3((n4 + 255) / 256), dim3(256), 0, s,
+                       (const float4 *)part, (float4 *)outf, n4, splits);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3((n4 + 255) / 256), dim3(256), 0, s,
+                       (const float4 *)part, (float4 *)outf, n4, splits);
   return hipGetLastError();
 }
 
 template <>
 hipError_t launch_gemm<bf16, f16>(int epi, const f16 *A, const bf16 *W, int M, int N, int K,
-                                  f16 *out, float *outf, hipStream_t s) {
-  return launch_mfma<f16>(epi, A, W, M, N, K, out, outf, s);
-}
-
-template <>
-hipError_t launch_gemm<bf16, bf16>(int epi, const bf16 *A, const bf16 *W, int M, int N, int K,
-                                   f16 *out, float *outf, hipStream_t s) {
-  return launch_mfma<bf16>(epi, A, W, M, N, K, out, outf, s);
+                                  f16 *out, float *outf, const GemmAux &aux, hipStream_t s) {
+  return launch_f16w_variant(-1, 0, epi, A, W, M, N, K, out, outf, aux.part, aux.part_cap,
+                             aux.cus, s);
 }
 
 template <>
 hipError_t launch_gemm<float, float>(int epi, const float *A, const float *W, int M, int N,
-                                     int K, float *out, float *outf, hipStream_t s) {
+                                     int K, float *out, float *outf, const GemmAux &,
+                                     hipStream_t s) {
   const dim3 grid((N + 63) / 64, (M + 63) / 64), block(256);
   switch (epi) {
     case EPI_STORE:
