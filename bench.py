@@ -61,7 +61,7 @@ def cpu_baseline(w, W, batch, n_sessions):
     Wh = type(W)(W.embed.cpu(), [{k: v.cpu() for k, v in lw.items()} for lw in W.layers],
                  W.final_norm.cpu(), W.lm_head.cpu())
     S = {b: int(batch.prefix_len[b]) for b in sess}
-    kv = {(l, b): (om.to_f64(batch.kv_k[l, b, :, :S[b]]), om.to_f64(batch.kv_v[l, b, :, :S[b]]))
+    kv = {(l, b): (om.k_prefix(batch.kv_k, l, b, S[b]), om.v_prefix(batch.kv_v, l, b, S[b]))
           for l in range(w.L) for b in sess}
     toks, pars = batch.tokens.cpu(), batch.parents.cpu()
     q = batch.q[: len(sess)].cpu().numpy().astype(np.float64)

@@ -78,14 +78,16 @@ typedef struct {
   const void *lm_head;                   /* [vocab, d_model]                           */
 } acespec_weights;
 
-/* KV cache, in the model dtype: k and v are each [n_layers][B][n_kv_heads][capacity]
- * [head_dim], keys stored after RoPE.  Slots [0, prefix_len[b]) hold session b's
- * verified context and are only read.  The verify call writes the tree's keys and
- * values into slots prefix_len[b] + r for tree rows r = 0..N (nothing is committed:
- * calling again with the same inputs gives the same result). */
+/* KV cache, in the model dtype.  Keys: k [n_layers][B][n_kv_heads][capacity][head_dim],
+ * stored after RoPE.  Values are head-dim-major: v [n_layers][B][n_kv_heads][head_dim]
+ * [capacity] (slot s of a head is column s), so that the attention's contraction over
+ * slots reads contiguous memory.  Slots [0, prefix_len[b]) hold session b's verified
+ * context and are only read.  The verify call writes the tree's keys and values into
+ * slots prefix_len[b] + r for tree rows r = 0..N (nothing is committed: calling again
+ * with the same inputs gives the same result). */
 typedef struct {
   void *k, *v;
-  int capacity;                 /* slots per (layer, session, kv head)                  */
+  int capacity;                 /* slots per (layer, session, kv head); multiple of 64 */
   const int32_t *prefix_len;    /* [B] DEVICE; needs prefix_len[b] + N + 1 <= capacity */
 } acespec_kv_cache;
 

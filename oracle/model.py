@@ -254,11 +254,22 @@ def path_to(parents: Sequence[int], r: int) -> List[int]:
 # ----------------------------------------------------------------------------------------
 
 
+def k_prefix(kv_k, l: int, b: int, S: int) -> np.ndarray:
+    """Keys of session b at layer l, slots [0, S): cache [L, B, Hkv, cap, hd] -> [Hkv, S, hd]."""
+    return to_f64(kv_k[l, b, :, :S])
+
+
+def v_prefix(kv_v, l: int, b: int, S: int) -> np.ndarray:
+    """Values of session b at layer l, slots [0, S): the value cache is head-dim-major,
+    [L, B, Hkv, hd, cap] -> [Hkv, S, hd]."""
+    return np.ascontiguousarray(to_f64(kv_v[l, b, :, :, :S]).transpose(0, 2, 1))
+
+
 def session_prefix(kv_k, kv_v, b: int, S: int):
     """Per-layer float64 copies of session b's cache prefix [Hkv, S, hd]."""
     L = kv_k.shape[0]
-    return ([to_f64(kv_k[l, b, :, :S]) for l in range(L)],
-            [to_f64(kv_v[l, b, :, :S]) for l in range(L)])
+    return ([k_prefix(kv_k, l, b, S) for l in range(L)],
+            [v_prefix(kv_v, l, b, S) for l in range(L)])
 
 
 def forward_tree_batch(weights, dims: Dims, tokens, parents, prefix_len, kv_prefix,

@@ -159,7 +159,8 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
                                   ctx->inv_freq, stream));
     int nsplit = 1;
     RUN(K_ATTN, launch_attention<T>(x_q, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
-                                    ctx->part_cap, B, n1, H, Hkv, hd, cap, stream, &nsplit));
+                                    ctx->part_cap, B, n1, H, Hkv, hd, cap, ctx->cus, stream,
+                                    &nsplit));
     RUN(K_GEMM_O, (launch_gemm<T, A>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
                                      ctx->x, aux, stream)));
     RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D,
@@ -396,6 +397,8 @@ int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespe
                 "N must be in [0, %d] (got %d)", ctx->max_nodes, N);
   if (kv->capacity < N + 1)
     return fail(ACESPEC_EINVAL, "kv capacity %d cannot hold the %d tree rows", kv->capacity, N + 1);
+  if (kv->capacity % 64 != 0)
+    return fail(ACESPEC_EINVAL, "kv capacity must be a multiple of 64 (got %d)", kv->capacity);
   int rc = check_params(p, d.vocab);
   if (rc) return rc;
   rc = check_outputs(o);

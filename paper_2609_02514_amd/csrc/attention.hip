@@ -6,37 +6,44 @@
 // values of tree row j sit in cache slot prefix_len + j, so one contiguous key range
 // [0, prefix_len + N + 1) covers everything and the mask applies to its tail only.
 //
-// bf16 model: one workgroup per (split, kv head, session).  The G query heads of the
-// kv head times the N+1 tree rows form the query rows (row = tree_row * G + head), in
-// 16-row MFMA tiles spread over the workgroup's waves.  The key range of the split is
-// streamed in 64-key chunks with coalesced 16-byte loads into LDS (keys XOR-swizzled,
-// values with a padded row stride), converted from the bf16 cache to fp16 on the way
-// (exact in the fp16 normal range); the next chunk's loads are in flight while the
-// current chunk is processed.  Queries arrive in fp16.  S = Q K^T and O += P V use
-// v_mfma_f32_16x16x32_f16 with fp32 accumulation and an online softmax in base 2; P
-// (in [0, 1]) is rounded to fp16 and goes through a per-wave LDS tile to become an MFMA
-// operand.  With several splits, unnormalised partial outputs
-// and (max, sum) pairs are merged by a small combine kernel.
+// bf16 model.  One workgroup of 8 waves per (key split, kv head, session).  Query rows
+// are the G query heads of the kv head times the N+1 tree rows (row = tree_row * G +
+// head), in 16-row tiles dealt round-robin to the waves (tile = wave + 8 t).  The key
+// range of the split streams through LDS in chunks of 64 slots:
+//  * HBM -> LDS by direct DMA (global_load_lds, 16 bytes a lane) into a ring of NST
+//    stages.  A stage holds the chunk's keys as [64 slots][head_dim] and its values,
+//    read from the head-dim-major value cache, as [head_dim][64 slots].  The 16-byte
+//    pieces of every row are XOR-swizzled so that the fragment reads below hit distinct
+//    banks; the DMA fixes where each lane's bytes land, so the swizzle is applied to the
+//    global source addresses.
+//  * One chunk ahead of its use, every thread widens its share of the stage from bf16
+//    to fp16 in place (exact in the fp16 normal range), so the MFMAs run on fp16
+//    operands like the rest of the pass, and zeroes the value columns past the last
+//    tree slot (their probability is 0, but 0 * NaN would not be).
+//  * Scores are computed transposed, S^T = K Q^T with v_mfma_f32_16x16x32_f16 (16 keys
+//    as rows, 16 queries as columns), so each lane holds 16 scores of ONE query.  The
+//    tree mask, the running max (reduced over the query's 4 lanes by two shuffles) and
+//    exp2 stay in the lane, and the lane's probabilities, rounded to fp16, are exactly
+//    its B operand of O^T = V^T P^T: the contraction order over the chunk's keys is a
+//    permutation shared with the V fragments (two 8-byte LDS reads a lane).  The O^T
+//    accumulator lane holds 4 head dims of its query, so the online-softmax rescale is
+//    lane-local (and skipped when no running max moved).
+//  * Barrier protocol at chunk c: a wave waits for its own DMA of chunk c+1; one LDS
+//    barrier then certifies that chunk c+1 landed for every wave, that every wave
+//    widened its share of chunk c, and that chunk c-1 is consumed, so its stage takes the
+//    DMA of chunk c+NST-1.  NST-2 chunks are in flight while chunk c is computed.
+//  With several splits, unnormalised partial outputs and (max, sum) pairs are merged by
+//  a small combine kernel.
 //
 // fp32 kernel (tiny models): one wave per (tree row, query head), keys in sequence.
 #include "common.h"
 
 namespace {
 
-constexpr int KC = 64;            // keys per chunk
+constexpr int KC = 64;            // slots per chunk
+constexpr int NWAVES = 8;         // waves per workgroup
 constexpr float LOG2E = 1.4426950408889634f;
-
-template <int HD>
-struct AttnSmem {
-  static constexpr int VSTRIDE = HD + 2;                   // fp16 elements per V row
-  f16 k[KC * HD];
-  f16 v[KC * VSTRIDE];
-};
-
-template <int HD>
-AS_DEVICE int kswz(int key, int chunk) {  // 16-byte chunk index swizzled within the row
-  return key * HD + ((chunk ^ (key & 7)) << 3);
-}
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
 AS_DEVICE bool tree_visible(int slot, int S, int n1, uint64_t anc) {
   if (slot < S) return true;
@@ -45,224 +52,246 @@ AS_DEVICE bool tree_visible(int slot, int S, int n1, uint64_t anc) {
   return j == 0 || ((anc >> (j - 1)) & 1ull);
 }
 
-constexpr int NWAVES = 8;  // waves per workgroup (tiles are dealt to them in order)
+// Element offset of 16-byte piece `piece` of key row `key` in a stage's K part.  A key
+// row is HD * 2 bytes; the swizzle spreads 16 consecutive keys over the 16 distinct
+// 16-byte bank groups of a 256-byte window.
+template <int HD> AS_DEVICE int k_off(int key, int piece) {
+  const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
+  return key * HD + ((piece ^ sw) << 3);
+}
+// Element offset of piece `piece` (8 slots) of head-dim row `row` in a stage's V^T part
+// (rows of 64 slots = 128 bytes, two rows per 256-byte window).
+AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ ((row >> 1) & 7)) << 3); }
 
-template <int HD, int TPW>
+// DMA of one chunk (keys key0 .. key0 + 63) into a stage: HD/8 blocks of 1 KB for K and
+// as many for V^T, spread over the 8 waves.
+template <int HD>
+AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int key0,
+                           int capacity, int wave, int lane) {
+  constexpr int BLOCKS = HD / 8;
+#pragma unroll
+  for (int j = 0; j < BLOCKS / NWAVES; ++j) {
+    const int i = wave + NWAVES * j;
+    const int e = i * 512 + lane * 8;          // element offset this lane's bytes land at
+    const int key = e / HD, piece = (e % HD) >> 3;
+    const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
+    dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ sw) << 3), (lds_ptr_t)(stage + i * 512));
+  }
+#pragma unroll
+  for (int j = 0; j < BLOCKS / NWAVES; ++j) {
+    const int i = wave + NWAVES * j;
+    const int row = i * 8 + (lane >> 3), piece = lane & 7;
+    dma16(vb + (size_t)row * capacity + key0 + ((piece ^ ((row >> 1) & 7)) << 3),
+          (lds_ptr_t)(stage + KC * HD + i * 512));
+  }
+}
+
+// bf16 -> fp16 in place for this thread's pieces of a stage; value slots >= total are
+// zeroed.
+template <int HD>
+AS_DEVICE void widen_chunk(uint16_t *stage, int tid, int key0, int total) {
+  constexpr int KPIECES = KC * HD / 8;
+  constexpr int PER = 2 * KPIECES / (NWAVES * 64);
+  const bool tail = key0 + KC > total;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int pc = tid + j * NWAVES * 64;
+    uint16_t *p = stage + pc * 8;
+    f16x8 h = bf16x8_to_f16x8(*(const bf16x8 *)p);
+    if (tail && pc >= KPIECES) {
+      const int vp = pc - KPIECES, row = vp >> 3;
+      const int s0 = key0 + (((vp & 7) ^ ((row >> 1) & 7)) << 3);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (s0 + e >= total) h[e] = (f16)0.f;
+    }
+    *(f16x8 *)p = h;
+  }
+}
+
+template <int HD, int TPW, int NST>
 __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
     const f16 *__restrict__ qin, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
     TreeMeta meta, f16 *__restrict__ out, float *__restrict__ part_o,
     float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit) {
-  constexpr int KSTEPS = HD / 32, NB = HD / 16, PSTRIDE = KC + 8;
-  constexpr int VST = AttnSmem<HD>::VSTRIDE;
-  __shared__ __attribute__((aligned(16))) AttnSmem<HD> sm;
-  __shared__ __attribute__((aligned(16))) f16 sP[NWAVES][16 * PSTRIDE];
+  constexpr int KSTEPS = HD / 32, NB = HD / 16;
+  constexpr int STAGE = 2 * KC * HD;     // elements: K [KC][HD], then V^T [HD][KC]
+  constexpr int L_DMA = HD / 32;         // DMA instructions per wave per chunk
+  static_assert(NST >= 3, "the widening runs one stage ahead of the MFMAs");
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
 
   const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int G = H / Hkv, QR = G * n1;
   const int ntiles = (QR + 15) / 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15, lk = lane >> 4;
-  const bool active = wave * TPW < ntiles;
+  const int lr = lane & 15, lg = lane >> 4;
   const int S = meta.sess_S[b];
   const int total = S + n1;
   const int nchunks = (total + KC - 1) / KC;
   const int cps = (nchunks + nsplit - 1) / nsplit;
-  const int c_begin = split * cps;
-  const int c_end = min(nchunks, c_begin + cps);
-  const size_t kvbase = ((size_t)b * Hkv + g) * capacity * HD;
+  const int c0 = split * cps;
+  const int c1 = min(nchunks, c0 + cps);
+  const bf16 *kb = ck + ((size_t)b * Hkv + g) * capacity * HD;
+  const bf16 *vb = cv + ((size_t)b * Hkv + g) * HD * capacity;
   const size_t row0 = (size_t)b * n1;
   const int q_stride = H * HD;
-  const float sscale = LOG2E / sqrtf((float)HD);
+  const float sscale = LOG2E / sqrtf((float)HD);   // scores -> base-2 exponent
 
-  // Query fragments (A operand of S = Q K^T) and running softmax state.
+  // Query fragments (B operand of S^T = K Q^T), tree-ancestor masks, softmax state.
   f16x8 qf[TPW][KSTEPS];
+  uint64_t anc[TPW];
+  float m_run[TPW], l_run[TPW];
   f32x4 o[TPW][NB];
-  float m_run[TPW][4], l_run[TPW][4];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
-    const int tile = wave * TPW + t;
-    int qi = tile * 16 + lr;
+    int qi = (wave + NWAVES * t) * 16 + lr;
     qi = qi < QR ? qi : QR - 1;
     const int r = qi / G, h = g * G + (qi - r * G);
     const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) qf[t][s] = *(const f16x8 *)(qp + s * 32 + lk * 8);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      m_run[t][e] = -INFINITY;
-      l_run[t][e] = 0.f;
-    }
+    for (int s = 0; s < KSTEPS; ++s) qf[t][s] = *(const f16x8 *)(qp + s * 32 + lg * 8);
+    anc[t] = meta.anc[row0 + r];
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) o[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  wait_vmcnt<0>();   // the loop's vmcnt accounting covers the DMA only
 
-  // Chunk staging: KC*HD/8 pieces of 16 bytes per operand.
-  constexpr int PIECES = KC * HD / 8;
-  constexpr int PPT = PIECES / (NWAVES * 64);
-  bf16x8 rk[PPT], rv[PPT];
-  auto load_chunk = [&](int c) {
-    const int key0 = c * KC;
+  auto stage_of = [&](int c) { return smem + ((c - c0) % NST) * STAGE; };
+
+  // Prologue: chunks c0 .. c0+NST-2 in flight, chunk c0 widened.
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int p = tid + i * NWAVES * 64;
-      const int key = p / (HD / 8), ch = p - key * (HD / 8);
-      int slot = key0 + key;
-      slot = slot < capacity ? slot : capacity - 1;
-      rk[i] = *(const bf16x8 *)(ck + kvbase + (size_t)slot * HD + ch * 8);
-      rv[i] = *(const bf16x8 *)(cv + kvbase + (size_t)slot * HD + ch * 8);
-    }
-  };
-  auto store_chunk = [&]() {
-#pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int p = tid + i * NWAVES * 64;
-      const int key = p / (HD / 8), ch = p - key * (HD / 8);
-      *(f16x8 *)(&sm.k[kswz<HD>(key, ch)]) = bf16x8_to_f16x8(rk[i]);
-      const f16x8 v16 = bf16x8_to_f16x8(rv[i]);
-      uint32_t *vd = (uint32_t *)(&sm.v[key * VST + ch * 8]);
-      const uint32_t *vs = (const uint32_t *)(&v16);
-      vd[0] = vs[0];
-      vd[1] = vs[1];
-      vd[2] = vs[2];
-      vd[3] = vs[3];
-    }
-  };
+  for (int i = 0; i < NST - 1; ++i)
+    if (c0 + i < c1) issue_chunk<HD>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
+  if (c0 < c1) {
+    if (c0 + NST - 2 < c1) wait_vmcnt<(NST - 2) * L_DMA>(); else wait_vmcnt<0>();
+    lds_barrier();
+    widen_chunk<HD>(stage_of(c0), tid, c0 * KC, total);
+  }
 
-  if (c_begin < c_end) load_chunk(c_begin);
-  f16 *myP = sP[wave];
-  for (int c = c_begin; c < c_end; ++c) {
-    __syncthreads();  // previous chunk fully consumed
-    store_chunk();
-    __syncthreads();
-    if (c + 1 < c_end) load_chunk(c + 1);
-    if (!active) continue;
+  for (int c = c0; c < c1; ++c) {
+    if (c + 1 < c1) {
+      if (c + NST - 2 < c1) wait_vmcnt<(NST - 3) * L_DMA>(); else wait_vmcnt<0>();
+    }
+    lds_barrier();
+    if (c + NST - 1 < c1)
+      issue_chunk<HD>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity, wave, lane);
+    if (c + 1 < c1) widen_chunk<HD>(stage_of(c + 1), tid, (c + 1) * KC, total);
+
+    const uint16_t *st = stage_of(c);
+    const f16 *sk = (const f16 *)st;
+    const f16 *sv = (const f16 *)(st + KC * HD);
     const int key0 = c * KC;
-    const bool tree_chunk = key0 + KC > S;  // chunk reaches the tree slots: apply the mask
-
+    const bool tree_chunk = key0 + KC > S;
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
-      const int tile = wave * TPW + t;
-      if (tile >= ntiles) break;
-      // S = Q K^T for 4 blocks of 16 keys.
+      if (wave + NWAVES * t >= ntiles) break;
+      // S^T for 4 blocks of 16 keys: sc[kb][e] is the score of slot key0 + kb*16 + lg*4
+      // + e against this lane's query.
       f32x4 sc[4];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int k4 = 0; k4 < 4; ++k4) sc[k4] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < KSTEPS; ++s) {
-          const f16x8 kf = *(const f16x8 *)(&sm.k[kswz<HD>(kb * 16 + lr, s * 4 + lk)]);
-          sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(qf[t][s], kf, sc[kb], 0, 0, 0);
+      for (int s = 0; s < KSTEPS; ++s)
+#pragma unroll
+        for (int k4 = 0; k4 < 4; ++k4) {
+          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(k4 * 16 + lr, s * 4 + lg));
+          sc[k4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[k4], 0, 0, 0);
         }
-      }
-      // Scale, mask (tree slots only), running max.  sc[kb][e] is the score of query row
-      // tile*16 + lk*4 + e against key key0 + kb*16 + lr.
-      uint64_t anc[4] = {~0ull, ~0ull, ~0ull, ~0ull};
       if (tree_chunk) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          int qo = tile * 16 + lk * 4 + e;
-          qo = qo < QR ? qo : QR - 1;
-          anc[e] = meta.anc[row0 + qo / G];
-        }
+        for (int k4 = 0; k4 < 4; ++k4)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            // slot key0 + k4*16 + lg*4 + e is tree row j (prefix slot if j < 0)
+            const int j = key0 + k4 * 16 + lg * 4 + e - S;
+            const int sh = min(max(j - 1, 0), 63);
+            const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((anc[t] >> sh) & 1ull)));
+            sc[k4][e] = vis ? sc[k4][e] : -INFINITY;
+          }
       }
-      float mx[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int slot = key0 + kb * 16 + lr;
+      for (int k4 = 0; k4 < 4; ++k4)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float v = sc[kb][e] * sscale;
-          if (tree_chunk && !tree_visible(slot, S, n1, anc[e])) v = -INFINITY;
-          sc[kb][e] = v;
-          mx[e] = fmaxf(mx[e], v);
-        }
-      }
-      float alpha[4], mref[4];
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[k4][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run[t], mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      // raw v_exp_f32: results below 2^-126 flush to zero, which a softmax weight can spare
+      const float alpha = __builtin_amdgcn_exp2f((m_run[t] - m_use) * sscale);
+      m_run[t] = m_new;
+      const float mb = m_use * sscale;
+      f16x8 pb[2];
+      float rs = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float v = mx[e];
-        v = fmaxf(v, __shfl_xor(v, 1));
-        v = fmaxf(v, __shfl_xor(v, 2));
-        v = fmaxf(v, __shfl_xor(v, 4));
-        v = fmaxf(v, __shfl_xor(v, 8));
-        const float mnew = fmaxf(m_run[t][e], v);
-        mref[e] = mnew == -INFINITY ? 0.f : mnew;
-        alpha[e] = exp2f(m_run[t][e] - mref[e]);
-        m_run[t][e] = mnew;
-      }
-      float rs[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
+      for (int k4 = 0; k4 < 4; ++k4)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const f16 pb = (f16)exp2f(sc[kb][e] - mref[e]);
-          rs[e] += (float)pb;
-          myP[(lk * 4 + e) * PSTRIDE + kb * 16 + lr] = pb;
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[k4][e], sscale, -mb));
+          rs += p;
+          pb[k4 >> 1][(k4 & 1) * 4 + e] = (f16)p;
         }
+      l_run[t] = l_run[t] * alpha + rs;
+      if (__ballot(alpha < 1.f)) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[t][nb][e] *= alpha;
       }
+      // O^T += V^T P^T over two k-steps of 32 keys.
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float v = rs[e];
-        v += __shfl_xor(v, 1);
-        v += __shfl_xor(v, 2);
-        v += __shfl_xor(v, 4);
-        v += __shfl_xor(v, 8);
-        l_run[t][e] = l_run[t][e] * alpha[e] + v;
-      }
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[t][nb][e] *= alpha[e];
-
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      // O += P V over two k-steps of 32 keys.  Both operands use key = s2*32 + lk*8 + j.
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const f16x8 pa = *(const f16x8 *)(&myP[lr * PSTRIDE + s2 * 32 + lk * 8]);
+      for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          f16x8 vb;
-          const f16 *vcol = &sm.v[(s2 * 32 + lk * 8) * VST + nb * 16 + lr];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) vb[j] = vcol[j * VST];
-          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pa, vb, o[t][nb], 0, 0, 0);
+          const int row = nb * 16 + lr;
+          const f16x4 lo = *(const f16x4 *)(sv + v_off(row, s2 * 4 + (lg >> 1)) + (lg & 1) * 4);
+          const f16x4 hi = *(const f16x4 *)(sv + v_off(row, s2 * 4 + 2 + (lg >> 1)) + (lg & 1) * 4);
+          const f16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[s2], o[t][nb], 0, 0, 0);
         }
-      }
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
   }
-  if (!active) return;
+  wait_vmcnt<0>();
 
-  // Output: o[t][nb][e] is row tile*16 + lk*4 + e, dim nb*16 + lr.
+  // o[t][nb][e] is head dim nb*16 + lg*4 + e of query tile*16 + lr.
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
-    const int tile = wave * TPW + t;
+    const int tile = wave + NWAVES * t;
     if (tile >= ntiles) break;
+    float l = l_run[t];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    const int qi = tile * 16 + lr;
+    if (qi >= QR) continue;
+    const int r = qi / G, h = g * G + (qi - r * G);
+    if (nsplit == 1) {
+      const float inv = l > 0.f ? 1.0f / l : 0.f;
+      f16 *op = out + (row0 + r) * (size_t)q_stride + h * HD + lg * 4;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int qi = tile * 16 + lk * 4 + e;
-      if (qi >= QR) continue;
-      const int r = qi / G, h = g * G + (qi - r * G);
-      if (nsplit == 1) {
-        const float inv = l_run[t][e] > 0.f ? 1.0f / l_run[t][e] : 0.f;
-        f16 *op = out + (row0 + r) * (size_t)(H * HD) + h * HD;
+      for (int nb = 0; nb < NB; ++nb) {
+        f16x4 v;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) op[nb * 16 + lr] = (f16)(o[t][nb][e] * inv);
-      } else {
-        const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
-        float *po = part_o + (item * QR + qi) * HD;
+        for (int e = 0; e < 4; ++e) v[e] = (f16)(o[t][nb][e] * inv);
+        *(f16x4 *)(op + nb * 16) = v;
+      }
+    } else {
+      const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
+      float *po = part_o + (item * QR + qi) * HD + lg * 4;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) po[nb * 16 + lr] = o[t][nb][e];
-        if (lr == 0) {
-          part_ml[(item * QR + qi) * 2 + 0] = m_run[t][e];
-          part_ml[(item * QR + qi) * 2 + 1] = l_run[t][e];
-        }
+      for (int nb = 0; nb < NB; ++nb) *(f32x4 *)(po + nb * 16) = o[t][nb];
+      if (lg == 0) {
+        part_ml[(item * QR + qi) * 2 + 0] = m_run[t] == -INFINITY ? -INFINITY : m_run[t] * sscale;
+        part_ml[(item * QR + qi) * 2 + 1] = l;
       }
     }
   }
 }
 
 // Merge of the split partials: one block per (kv head, session), one thread per value.
+// part_ml holds (max in base-2 exponent units, sum) per (item, query row).
 template <typename T>
 __global__ void attn_combine_kernel(const float *__restrict__ part_o,
                                     const float *__restrict__ part_ml, T *__restrict__ out,
@@ -298,20 +327,20 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(
   const uint64_t anc = meta.anc[row];
   const float *q = qin + (size_t)row * H * HD + h * HD;
   const float q0 = lane < HD ? q[lane] : 0.f, q1 = lane + 64 < HD ? q[lane + 64] : 0.f;
-  const size_t kvbase = ((size_t)b * Hkv + g) * capacity * HD;
+  const float *kb = ck + ((size_t)b * Hkv + g) * capacity * HD;
+  const float *vb = cv + ((size_t)b * Hkv + g) * HD * capacity;   // [HD][capacity]
   const float scale = 1.0f / sqrtf((float)HD);
   float m = -INFINITY, l = 0.f, o0 = 0.f, o1 = 0.f;
   for (int slot = 0; slot < S + n1; ++slot) {
     if (!tree_visible(slot, S, n1, anc)) continue;
-    const float *k = ck + kvbase + (size_t)slot * HD;
-    const float *v = cv + kvbase + (size_t)slot * HD;
+    const float *k = kb + (size_t)slot * HD;
     float part = (lane < HD ? q0 * k[lane] : 0.f) + (lane + 64 < HD ? q1 * k[lane + 64] : 0.f);
     const float s = wave_sum(part) * scale;
     const float mn = fmaxf(m, s);
     const float a = expf(m - mn), p = expf(s - mn);
     l = l * a + p;
-    o0 = o0 * a + p * (lane < HD ? v[lane] : 0.f);
-    o1 = o1 * a + p * (lane + 64 < HD ? v[lane + 64] : 0.f);
+    o0 = o0 * a + p * (lane < HD ? vb[(size_t)lane * capacity + slot] : 0.f);
+    o1 = o1 * a + p * (lane + 64 < HD ? vb[(size_t)(lane + 64) * capacity + slot] : 0.f);
     m = mn;
   }
   float *op = out + (size_t)row * (H * HD) + h * HD;
@@ -319,12 +348,17 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(
   if (lane + 64 < HD) op[lane + 64] = o1 / l;
 }
 
+// Ring depth per head dim: 4 stages of 32 KB (head_dim 128, one workgroup per CU) or of
+// 16 KB (head_dim 64, two per CU).
+template <int HD> struct AttnCfg { static constexpr int NST = 4; };
+
 template <int HD, int TPW>
 void launch_mfma(dim3 grid, hipStream_t s, const f16 *q, const bf16 *ck, const bf16 *cv,
                  const TreeMeta &meta, f16 *out, float *po, float *pml, int n1, int H, int Hkv,
                  int capacity, int nsplit) {
-  hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, TPW>), grid, dim3(NWAVES * 64), 0, s, q, ck, cv,
-                     meta, out, po, pml, n1, H, Hkv, capacity, nsplit);
+  hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, TPW, AttnCfg<HD>::NST>), grid,
+                     dim3(NWAVES * 64), 0, s, q, ck, cv, meta, out, po, pml, n1, H, Hkv,
+                     capacity, nsplit);
 }
 
 }  // namespace
@@ -335,18 +369,19 @@ template <>
 hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
                                   const TreeMeta &meta, f16 *out, float *part_o,
                                   float *part_ml, long long part_capacity, int B, int n1, int H,
-                                  int Hkv, int hd, int capacity, hipStream_t s,
+                                  int Hkv, int hd, int capacity, int cus, hipStream_t s,
                                   int *nsplit_used) {
   const int G = H / Hkv, QR = G * n1;
   const int tiles = (QR + 15) / 16;
   const int tpw = (tiles + NWAVES - 1) / NWAVES;
-  if (tpw > 4) return hipErrorInvalidValue;
-  // Splits over the key range so that the launch has enough workgroups to fill the
-  // chip, keeping at least 8 chunks (512 keys) per split.
+  if (tpw > 4 || capacity % KC != 0) return hipErrorInvalidValue;
+  // Key splits so that every resident workgroup slot of the chip gets work (one
+  // workgroup per CU at head_dim 128, two at 64), keeping at least 4 chunks per split.
+  const int slots = cus * (hd == 128 ? 1 : 2);
   const int items = B * Hkv;
-  const int nchunks = (capacity + KC - 1) / KC;
-  int nsplit = (512 + items - 1) / items;
-  nsplit = nsplit < nchunks / 8 ? nsplit : nchunks / 8;
+  const int nchunks = capacity / KC;
+  int nsplit = (slots + items - 1) / items;
+  nsplit = nsplit < nchunks / 4 ? nsplit : nchunks / 4;
   if (nsplit < 1) nsplit = 1;
   while (nsplit > 1 && (long long)items * nsplit * QR * hd > part_capacity) --nsplit;
   *nsplit_used = nsplit;
@@ -371,7 +406,7 @@ template <>
 hipError_t launch_attention<float>(const float *q, const float *ck, const float *cv,
                                    const TreeMeta &meta, float *out, float *, float *,
                                    long long, int B, int n1, int H, int Hkv, int hd,
-                                   int capacity, hipStream_t s, int *nsplit_used) {
+                                   int capacity, int, hipStream_t s, int *nsplit_used) {
   *nsplit_used = 1;
   hipLaunchKernelGGL(tree_attn_f32_kernel, dim3(H, B * n1), dim3(64), 0, s, q, ck, cv, meta,
                      out, n1, H, Hkv, hd, capacity);

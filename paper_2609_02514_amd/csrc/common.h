@@ -62,6 +62,34 @@ AS_DEVICE int wave_sum_i32(int v) {
 }
 
 // ------------------------------------------------------------------------------------
+// Direct global -> LDS staging (gfx950)
+// ------------------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+// One wave copies 64 x 16 bytes: lane i reads its own global address g and the bytes land
+// at l + 16 i (l is wave-uniform).  Completion is counted by vmcnt like any load.
+AS_DEVICE void dma16(const void *g, lds_ptr_t l) {
+  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+}
+
+// Waits until at most VM vector-memory loads of this wave are outstanding (leaves the
+// LDS and export counters alone).
+template <int VM> AS_DEVICE void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier that orders LDS accesses only: unlike __syncthreads() it does not
+// drain outstanding global loads, so DMA into other stages stays in flight.
+AS_DEVICE void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// ------------------------------------------------------------------------------------
 // Tree metadata produced by the tree-prep kernel (one entry per tree row)
 // ------------------------------------------------------------------------------------
 struct TreeMeta {
@@ -96,7 +124,8 @@ hipError_t launch_rmsnorm(const TIN *x, const TW *gain, typename ActOf<TW>::type
                           int d, float eps, hipStream_t s);
 
 // RoPE on q and k of the fp32 QKV projection; q goes to q_out (activation type,
-// [rows, H*hd]), k and v to the cache slots of the tree rows.
+// [rows, H*hd]), k and v to the cache slots of the tree rows (keys [B][Hkv][cap][hd],
+// values head-dim-major [B][Hkv][hd][cap]).
 template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
@@ -135,7 +164,7 @@ hipError_t launch_attention(const typename ActOf<TW>::type *q, const TW *cache_k
                             const TW *cache_v, const TreeMeta &meta,
                             typename ActOf<TW>::type *out, float *part_o, float *part_ml,
                             long long part_capacity, int B, int n1, int H, int Hkv, int hd,
-                            int capacity, hipStream_t s, int *nsplit_used);
+                            int capacity, int cus, hipStream_t s, int *nsplit_used);
 
 struct VocabArgs {
   const float *logits;      // [rows, V]

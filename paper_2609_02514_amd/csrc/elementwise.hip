@@ -71,11 +71,12 @@ __global__ void rope_kv_kernel(const float *__restrict__ qkv, TA *__restrict__ q
     const float *k = base + (H + g) * hd;
     const float *v = base + (H + Hkv + g) * hd;
     const float x1 = k[i], x2 = k[i + half];
-    const size_t dst = (((size_t)b * Hkv + g) * capacity + slot) * hd;
-    ck[dst + i] = from_f32<TW>(x1 * c - x2 * s);
-    ck[dst + i + half] = from_f32<TW>(x2 * c + x1 * s);
-    cv[dst + i] = from_f32<TW>(v[i]);
-    cv[dst + i + half] = from_f32<TW>(v[i + half]);
+    const size_t kdst = (((size_t)b * Hkv + g) * capacity + slot) * hd;
+    ck[kdst + i] = from_f32<TW>(x1 * c - x2 * s);
+    ck[kdst + i + half] = from_f32<TW>(x2 * c + x1 * s);
+    const size_t vdst = ((size_t)b * Hkv + g) * hd * capacity + slot;   // [hd][capacity]
+    cv[vdst + (size_t)i * capacity] = from_f32<TW>(v[i]);
+    cv[vdst + (size_t)(i + half) * capacity] = from_f32<TW>(v[i + half]);
   }
 }
 

@@ -49,20 +49,9 @@ AS_DEVICE int xcd_tile(int bid, int total) {
 // ------------------------------------------------------------------------------------
 constexpr int KS = 32;  // k per stage
 
-typedef __attribute__((address_space(3))) void *lds_ptr_t;
-
-AS_DEVICE void dma16(const void *g, lds_ptr_t l) {
-  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
-}
 // 64-byte rows, 16-byte chunks swizzled by (row >> 1) & 3; returns an element offset.
 AS_DEVICE int swz32(int row, int chunk) { return row * KS + ((chunk ^ ((row >> 1) & 3)) << 3); }
 
-template <int VM> AS_DEVICE void wait_vmcnt() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
 
 template <int EPI, int WMN, int WNN, int WTM, int WTN, int NST, int OCC>
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(

@@ -17,7 +17,8 @@ stand in for them):
 * Weights ~ N(0, 0.02) drawn in fp32 and rounded once (RNE) to the model
   dtype; RMSNorm gains are 1.0 unless ``random_gains`` is set.
 * KV prefix ~ N(0, 1), already rotated (keys are stored post-RoPE), in the
-  model dtype.  No prefill is run.
+  model dtype.  No prefill is run.  Cache layout: keys [L, B, Hkv, cap, hd], values
+  head-dim-major [L, B, Hkv, hd, cap]; cap is a multiple of 64.
 * Draft distributions q = softmax(g / T_q) with g ~ N(0, q_std) per row.
 * Trees follow the drafter of the paper (Section III-C): at each parent the
   main child is sampled from q of that parent and the siblings are the top-F
@@ -257,7 +258,7 @@ class Batch:
     parents: torch.Tensor         # [B, N+1] int32
     prefix_len: torch.Tensor      # [B] int32
     kv_k: Optional[torch.Tensor]  # [L, B, Hkv, cap, hd]
-    kv_v: Optional[torch.Tensor]
+    kv_v: Optional[torch.Tensor]  # [L, B, Hkv, hd, cap]
     q: torch.Tensor               # [B, N+1, V] fp32
     u: torch.Tensor               # [B, N+1, 3] fp32
     cap: int = 0
@@ -275,12 +276,13 @@ def prefix_lengths(w: Workload, seed: int) -> List[int]:
 
 def make_kv(w: Workload, device, seed: int, cap: int):
     dt = _torch_dtype(w)
-    shape = (w.L, w.B, w.Hkv, cap, w.hd)
-    k = torch.empty(shape, dtype=dt, device=device)
-    v = torch.empty(shape, dtype=dt, device=device)
+    kshape = (w.L, w.B, w.Hkv, cap, w.hd)
+    vshape = (w.L, w.B, w.Hkv, w.hd, cap)
+    k = torch.empty(kshape, dtype=dt, device=device)
+    v = torch.empty(vshape, dtype=dt, device=device)
     for l in range(w.L):   # per layer, to bound the fp32 staging memory
-        k[l].copy_(normal(shape[1:], 1.0, dt, device, seed, 1, 2 * l))
-        v[l].copy_(normal(shape[1:], 1.0, dt, device, seed, 1, 2 * l + 1))
+        k[l].copy_(normal(kshape[1:], 1.0, dt, device, seed, 1, 2 * l))
+        v[l].copy_(normal(vshape[1:], 1.0, dt, device, seed, 1, 2 * l + 1))
     return k, v
 
 
@@ -322,7 +324,7 @@ def make_batch(w: Workload, device="cpu", seed: Optional[int] = None,
                 for j, c in enumerate(ch[r][1:]):
                     tok[:, c] = sib[:, j]
     S_list = prefix_lengths(w, seed)
-    cap = max(S_list) + n1 + extra_cap
+    cap = (max(S_list) + n1 + extra_cap + 63) // 64 * 64
     kv_k, kv_v = make_kv(w, device, seed, cap)
     return Batch(tokens=tok.to(torch.int32), parents=par.to(device),
                  prefix_len=torch.tensor(S_list, dtype=torch.int32, device=device),

@@ -64,8 +64,8 @@ def run_tree(w: synth.Workload, seed=None, sessions: Sequence[int] = None, devic
     # host copies BEFORE the HIP path runs (it writes the tree slots of the cache)
     hin = dict(tokens=host(batch.tokens), parents=host(batch.parents),
                prefix_len=host(batch.prefix_len), q=host(batch.q), u=host(batch.u),
-               kv={(l, b): (om.to_f64(batch.kv_k[l, b, :, :int(batch.prefix_len[b])]),
-                            om.to_f64(batch.kv_v[l, b, :, :int(batch.prefix_len[b])]))
+               kv={(l, b): (om.k_prefix(batch.kv_k, l, b, int(batch.prefix_len[b])),
+                            om.v_prefix(batch.kv_v, l, b, int(batch.prefix_len[b])))
                    for l in range(w.L) for b in sessions})
     v = verifier or Verifier.for_workload(w)
     ws = v.weights_struct(W)
