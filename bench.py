@@ -45,6 +45,106 @@ def kernel_work(w, B, n1, P, S_tot):
     }
 
 
+# ---------------------------------------------------------------------------------------
+# HBM traffic from rocprofv3 counters
+# ---------------------------------------------------------------------------------------
+CSRC = os.path.join(ROOT, "paper_2609_02514_amd", "csrc")
+# source files whose change invalidates a kernel kind's measured counters
+KIND_SOURCES = {
+    "tree_attention": ["attention.hip"], "gemm_qkv": ["gemm.hip"], "gemm_o": ["gemm.hip"],
+    "gemm_gate_up": ["gemm.hip"], "gemm_down": ["gemm.hip"], "gemm_lm_head": ["gemm.hip"],
+    "vocab_verify": ["vocab.hip"], "rmsnorm": ["elementwise.hip"], "rope_kv": ["elementwise.hip"],
+}
+
+
+def kind_source_hash(kind):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KIND_SOURCES.get(kind, []) + ["common.h"]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _pmc_rows(run_dir):
+    import csv
+    path = os.path.join(run_dir, "run_counter_collection.csv")
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def _label_dispatches(rows):
+    """Kernel kind of every dispatch of the verify library, from the symbol and the fixed
+    launch order of a step (per layer: QKV, O, gate/up, down; LM head right before the
+    vocabulary kernel)."""
+    labels, resid_seen = [], 0
+    for i, r in enumerate(rows):
+        n = r["Kernel_Name"]
+        kind = None
+        if "tree_attn_mfma_kernel" in n:
+            kind = "tree_attention"
+        elif "gemm_f16w_kernelILi2E" in n:
+            kind = "gemm_gate_up"
+        elif "gemm_f16w_kernelILi1E" in n:
+            kind = "gemm_o" if resid_seen % 2 == 0 else "gemm_down"
+            resid_seen += 1
+        elif "gemm_f16w_kernelILi3E" in n:
+            nxt = next((rows[j]["Kernel_Name"] for j in range(i + 1, len(rows))
+                        if "splitk_reduce" not in rows[j]["Kernel_Name"]), "")
+            kind = "gemm_lm_head" if "vocab_verify" in nxt else "gemm_qkv"
+        elif "vocab_verify_kernel" in n:
+            kind = "vocab_verify"
+        elif "rmsnorm_kernel" in n:
+            kind = "rmsnorm"
+        elif "rope_kv_kernel" in n:
+            kind = "rope_kv"
+        labels.append(kind)
+    return labels
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mib):
+    """Per-kind HBM bytes per launch: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    scaled by what the counter reads for a plain copy of copy_mib MiB."""
+    copy_kib = copy_mib * 1024.0
+    cf = sum(float(r["Counter_Value"]) for r in _pmc_rows(copy_fetch_dir))
+    cw = sum(float(r["Counter_Value"]) for r in _pmc_rows(copy_write_dir))
+    f_scale, w_scale = copy_kib / cf, copy_kib / cw
+    out = {"copy_mib": copy_mib, "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "kinds": {}}
+    acc = {}
+    for which, d in (("fetch", fetch_dir), ("write", write_dir)):
+        rows = _pmc_rows(d)
+        for kind, r in zip(_label_dispatches(rows), rows):
+            if kind is None:
+                continue
+            e = acc.setdefault(kind, {"fetch": [], "write": []})
+            e[which].append(float(r["Counter_Value"]))
+    for kind, e in sorted(acc.items()):
+        fk = sum(e["fetch"]) / max(len(e["fetch"]), 1)
+        wk = sum(e["write"]) / max(len(e["write"]), 1)
+        out["kinds"][kind] = {
+            "launches": len(e["fetch"]), "fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+            "hbm_bytes_per_launch": round((fk * f_scale + wk * w_scale) * 1024.0),
+            "source_sha": kind_source_hash(kind)}
+    return out
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per launch per kernel kind from the committed counter summary,
+    or {} -- a kind whose sources changed since the counters were taken is dropped."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return {}
+    text = open(path).read()
+    i = text.find("```json")
+    if i < 0:
+        return {}
+    blob = json.loads(text[i + 7: text.index("```", i + 7)])
+    return {k: v["hbm_bytes_per_launch"] for k, v in blob["kinds"].items()
+            if v.get("source_sha") == kind_source_hash(k)}
+
+
 def cpu_baseline(w, W, batch, n_sessions):
     """The oracle as it stands on n_sessions whole sessions: the tree forward through every
     layer, the verify stage of every row and the walk."""
@@ -91,10 +191,32 @@ def main():
     ap.add_argument("--workload", default="8b-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sessions", type=int, default=2)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run one plain device-to-device copy of MIB MiB (the reference "
+                         "kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="print the per-kernel HBM traffic summary of four rocprofv3 --pmc "
+                         "output directories (bench FETCH_SIZE, bench WRITE_SIZE, copy "
+                         "FETCH_SIZE, copy WRITE_SIZE)")
+    ap.add_argument("--copy-mib", type=int, default=1024)
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(*args.summarize_pmc, args.copy_mib), indent=1))
+        return
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.empty(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n * 4, "read_bytes": n * 4, "write_bytes": n * 4}))
+        return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus}); the verify step "
-              "shards by session with no collectives, see the design notes", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for {args.gpus}): the verify step "
+              "shards by session with no collectives, and only the one-GPU step is built "
+              "and measured", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -161,15 +283,21 @@ def main():
                 ent["gbs"] = round(by / (avg / 1e3) / 1e9, 1)
                 ent["hbm_frac"] = round(ent["gbs"] / PEAK_HBM_GBS, 4)
         kernels[name] = ent
+    traffic = load_traffic(w.name)
+    for name, ent in kernels.items():
+        if name in traffic:
+            ent["hbm_traffic_bytes_per_launch"] = traffic[name]
     dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
     if dom.startswith("gemm"):
         roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dk["mfma_frac"],
-                "traffic": None}
+                "traffic": traffic.get(dom)}
     else:
         roof = {"kernel": dom, "bound": "hbm", "achieved": dk["gbs"], "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": dk["hbm_frac"], "traffic": None}
+                "unit": "GB/s", "frac": dk["hbm_frac"], "traffic": traffic.get(dom)}
+    roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
+    roof["algorithmic_per_launch"] = {"flops": work[dom][0], "bytes": work[dom][1]} if dom in work else None
 
     cpu = None
     if not args.no_cpu_baseline:
