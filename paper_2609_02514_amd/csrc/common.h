@@ -72,6 +72,16 @@ AS_DEVICE void dma16(const void *g, lds_ptr_t l) {
   __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
 }
 
+// The same through a buffer resource: lane i reads rsrc + voff + soff (soff scalar, so a
+// moving k offset costs no vector arithmetic); reads past the resource's size return 0.
+AS_DEVICE void buf_dma16(__amdgpu_buffer_rsrc_t rsrc, lds_ptr_t l, uint32_t voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, l, 16, voff, soff, 0, 0);
+}
+AS_DEVICE __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
 // Waits until at most VM vector-memory loads of this wave are outstanding (leaves the
 // LDS and export counters alone).
 template <int VM> AS_DEVICE void wait_vmcnt() {
@@ -150,10 +160,12 @@ hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
                        typename ActOf<TW>::type *out, float *outf, const GemmAux &aux,
                        hipStream_t s);
 
-// The fp16 x bf16 GEMM with an explicit tiling (var >= 0) and split count
-// (splits_override > 0); var < 0 / splits_override <= 0 choose automatically.
+// The fp16-activation MFMA GEMM (weights TB = bf16, widened to fp16 in registers) with
+// an explicit tiling (var >= 0) and split count (splits_override > 0); var < 0 /
+// splits_override <= 0 choose automatically.
+template <typename TB>
 hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
-                               const bf16 *W, int M, int N, int K, f16 *out, float *outf,
+                               const TB *W, int M, int N, int K, f16 *out, float *outf,
                                float *part, long long part_cap, int cus, hipStream_t s);
 
 // Exact widening of a bf16 tensor to fp16 (in range), n elements.

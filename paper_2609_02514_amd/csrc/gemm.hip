@@ -22,6 +22,13 @@ namespace {
 
 AS_DEVICE float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
 
+// Weight fragments: fp16 weights are used as loaded, bf16 weights are widened to fp16.
+template <typename TB> struct Vec8;
+template <> struct Vec8<f16> { typedef f16x8 type; };
+template <> struct Vec8<bf16> { typedef bf16x8 type; };
+AS_DEVICE f16x8 to_f16(f16x8 v) { return v; }
+AS_DEVICE f16x8 to_f16(bf16x8 v) { return bf16x8_to_f16x8(v); }
+
 // Maps a workgroup id onto a tile id so that consecutive tile ids share an XCD.
 AS_DEVICE int xcd_tile(int bid, int total) {
   const int x = bid & 7, local = bid >> 3;
@@ -31,15 +38,17 @@ AS_DEVICE int xcd_tile(int bid, int total) {
 }
 
 // ------------------------------------------------------------------------------------
-// fp16 x bf16 MFMA kernel, templated on the tiling.
+// fp16-activation MFMA kernel, templated on the tiling.
 //   WMN x WNN waves; each owns a (WTM*16) x (WTN*16) output sub-tile made of 16 x 16 MFMA
-//   blocks, fp32 accumulators in AGPRs.  Block tile TBM x TBN, k-step 32 (64-byte rows).
-//   Operands move HBM -> LDS with gfx950's direct loads (global_load_lds_dwordx4: 64
-//   lanes x 16 bytes land contiguously at a wave-uniform LDS address) through a ring of
-//   NST stages, NST - 2 of them in flight.  The four 16-byte chunks of each 64-byte row
-//   are XOR-swizzled by ((row >> 1) & 3) so that the 16-byte fragment reads of 8
-//   consecutive rows hit 32 distinct banks; since the DMA fixes where each lane's bytes
-//   land, the swizzle is applied to the global source address.
+//   blocks (v_mfma_f32_16x16x32_f16), fp32 accumulators.  Block tile TBM x TBN, KSS
+//   k-values per stage (rows of 2*KSS bytes).  Operands move HBM -> LDS by direct
+//   buffer loads (buffer_load_dwordx4 ... lds: 64 lanes x 16 bytes land contiguously at a
+//   wave-uniform LDS address; the k offset of a stage is a scalar) through a ring of NST
+//   stages, NST - 2 of them in flight.  Full 128-byte rows (KSS = 64) move twice the bytes
+//   per cycle of 64-byte rows through the L2 -> LDS path.  The 16-byte pieces of every row
+//   are XOR-swizzled so that the 16 rows read by one 16-lane group of a fragment load
+//   hit 16 distinct bank groups; since the DMA fixes where each lane's bytes land, the
+//   swizzle is applied to the global source addresses.
 //   One barrier per stage, placed mid-stage: it certifies that the NEXT stage has landed
 //   for every wave and that the stage loaded NST - 1 ahead is free, so each wave reads
 //   the next stage's first fragments while its last MFMAs of the current stage run.  The
@@ -47,27 +56,31 @@ AS_DEVICE int xcd_tile(int bid, int total) {
 //   free stage; next-stage fragments are always read) so the compiler counts
 //   outstanding LDS reads exactly, and fragment reads are fenced against the MFMAs.
 // ------------------------------------------------------------------------------------
-constexpr int KS = 32;  // k per stage
+// Byte offset of 16-byte piece `pc` of row `row` in rows of ROWB bytes.
+template <int ROWB> AS_DEVICE int piece_off(int row, int pc) {
+  const int sw = (row / (256 / ROWB)) & (ROWB / 16 - 1);
+  return row * ROWB + ((pc ^ sw) << 4);
+}
 
-// 64-byte rows, 16-byte chunks swizzled by (row >> 1) & 3; returns an element offset.
-AS_DEVICE int swz32(int row, int chunk) { return row * KS + ((chunk ^ ((row >> 1) & 3)) << 3); }
-
-
-template <int EPI, int WMN, int WNN, int WTM, int WTN, int NST, int OCC>
+template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int OCC, int KSS>
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
-    const f16 *__restrict__ A, const bf16 *__restrict__ W, int M, int N, int K,
+    const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
     int splits) {
   constexpr int NW = WMN * WNN;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
-  constexpr int A_BYTES = TBM * KS * 2, B_BYTES = TBN * KS * 2;
+  constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
+  constexpr int A_BYTES = TBM * ROWB, B_BYTES = TBN * ROWB;
   constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   constexpr int A_DMA = A_BYTES / 1024 / NW, B_DMA = B_BYTES / 1024 / NW;
   constexpr int L_DMA = A_DMA + B_DMA;
+  constexpr int KSUB = KSS / 32;            // 32-wide MFMA k steps per stage
+  constexpr int F = KSUB * WTM;             // A fragments per stage, in use order
   static_assert(A_DMA * 1024 * NW == A_BYTES && B_DMA * 1024 * NW == B_BYTES, "DMA split");
-  static_assert(WTM >= 4 && NST >= 3, "pipeline shape");
+  static_assert(F >= 4 && NST >= 3, "pipeline shape");
   constexpr int HALF = WTN / 2;  // SwiGLU: gate blocks, then the matching up blocks
-  __shared__ __attribute__((aligned(16))) char smem[NST * STAGE_BYTES];
+  __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE_BYTES];
+  typedef typename Vec8<TB>::type tbx8;
 
   const int units = mt * nt * splits;
   const int unit = xcd_tile(blockIdx.x, units);
@@ -75,27 +88,32 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   const int rem = unit - tn * (mt * splits);
   const int tm = rem / splits, sp = rem - tm * splits;
   const int m0 = tm * TBM;
-  const int KT = K / KS;
+  const int KT = K / KSS;
   const int kt0 = (int)((long long)KT * sp / splits), kt1 = (int)((long long)KT * (sp + 1) / splits);
   const int nk = kt1 - kt0;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w / WNN, wn = w - wm * WNN;
   const int lr = lane & 15, lk = lane >> 4;
 
-  // DMA sources: block j covers tile rows 16j..16j+15; lane l lands at row 16j + l/4,
-  // physical chunk l%4, which holds logical chunk (l%4) ^ ((row >> 1) & 3).
-  const int drow = lane >> 2, dchunk = (lane & 3) ^ ((lane >> 3) & 3);
-  const f16 *ga[A_DMA];
-  const bf16 *gb[B_DMA];
+  // DMA sources: block j of an operand covers tile rows ROWS_PER_BLK*j ..; lane l lands at
+  // row ROWS_PER_BLK*j + l / PIECES, physical piece l % PIECES.  Rows past M or N are
+  // clamped to the last row (their products are never stored).
+  const __amdgpu_buffer_rsrc_t rsa = make_rsrc(A, (uint32_t)((size_t)M * K * 2));
+  const int wrows = EPI == acespec::EPI_SWIGLU ? 2 * N : N;
+  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(W, (uint32_t)((size_t)wrows * K * 2));
+  const int drow = lane / PIECES, dpc = lane % PIECES;
+  uint32_t va[A_DMA], vb[B_DMA];
 #pragma unroll
   for (int t = 0; t < A_DMA; ++t) {
-    int r = m0 + (w * A_DMA + t) * 16 + drow;
+    const int lrow = (w * A_DMA + t) * ROWS_PER_BLK + drow;
+    int r = m0 + lrow;
     r = r < M ? r : M - 1;
-    ga[t] = A + (size_t)r * K + dchunk * 8;
+    va[t] = (uint32_t)r * K * 2 + (piece_off<ROWB>(lrow, dpc) - lrow * ROWB);
   }
 #pragma unroll
   for (int t = 0; t < B_DMA; ++t) {
-    const int row = (w * B_DMA + t) * 16 + drow;  // W-tile row
+    const int row = (w * B_DMA + t) * ROWS_PER_BLK + drow;  // W-tile row
     int wr;
     if (EPI == acespec::EPI_SWIGLU) {
       const int j = tn * (TBN / 2) + (row % (TBN / 2));
@@ -105,30 +123,34 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
       wr = tn * TBN + row;
       wr = wr < N ? wr : N - 1;
     }
-    gb[t] = W + (size_t)wr * K + dchunk * 8;
+    vb[t] = (uint32_t)wr * K * 2 + (piece_off<ROWB>(row, dpc) - row * ROWB);
   }
   auto issue = [&](int kt, int stage) {
     char *base = smem + stage * STAGE_BYTES;
-    const int koff = kt * KS;
+    const int soff = kt * ROWB;
 #pragma unroll
     for (int t = 0; t < A_DMA; ++t)
-      dma16(ga[t] + koff, (lds_ptr_t)(base + (w * A_DMA + t) * 1024));
+      buf_dma16(rsa, (lds_ptr_t)(base + (w * A_DMA + t) * 1024), va[t], soff);
 #pragma unroll
     for (int t = 0; t < B_DMA; ++t)
-      dma16(gb[t] + koff, (lds_ptr_t)(base + A_BYTES + (w * B_DMA + t) * 1024));
+      buf_dma16(rsb, (lds_ptr_t)(base + A_BYTES + (w * B_DMA + t) * 1024), vb[t], soff);
   };
 
-  int boff[WTN], aoff[WTM];
+  // Fragment byte offsets within a stage: A fragment f = (k step f / WTM, row block
+  // f % WTM); B fragment (k step s2, column block j).
+  int aoff[F], boff[KSUB][WTN];
+#pragma unroll
+  for (int f = 0; f < F; ++f)
+    aoff[f] = piece_off<ROWB>(wm * WTM * 16 + (f % WTM) * 16 + lr, (f / WTM) * 4 + lk);
 #pragma unroll
   for (int j = 0; j < WTN; ++j) {
     const int brow = (EPI == acespec::EPI_SWIGLU)
                          ? (j < HALF ? wn * HALF * 16 + j * 16
                                      : TBN / 2 + wn * HALF * 16 + (j - HALF) * 16) + lr
                          : wn * WTN * 16 + j * 16 + lr;
-    boff[j] = swz32(brow, lk);
-  }
 #pragma unroll
-  for (int ii = 0; ii < WTM; ++ii) aoff[ii] = swz32(wm * WTM * 16 + ii * 16 + lr, lk);
+    for (int s2 = 0; s2 < KSUB; ++s2) boff[s2][j] = A_BYTES + piece_off<ROWB>(brow, s2 * 4 + lk);
+  }
 
   f32x4 acc[WTM][WTN];
 #pragma unroll
@@ -139,45 +161,47 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   for (int p = 0; p < NST - 1; ++p) issue(kt0 + (p < nk ? p : nk - 1), p);
   wait_vmcnt<(NST - 2) * L_DMA>();  // stage 0 landed for this wave
   __builtin_amdgcn_s_barrier();
-  f16x8 fb[WTN], fa[WTM];
-  bf16x8 rbn[WTN];
-  {
-    const bf16 *sB = (const bf16 *)(smem + A_BYTES);
-    const f16 *sA = (const f16 *)smem;
+  f16x8 fb[KSUB][WTN], fa[F];
+  tbx8 rbn[KSUB][WTN];
 #pragma unroll
-    for (int j = 0; j < WTN; ++j) fb[j] = bf16x8_to_f16x8(*(const bf16x8 *)(&sB[boff[j]]));
-    fa[0] = *(const f16x8 *)(&sA[aoff[0]]);
-    fa[1] = *(const f16x8 *)(&sA[aoff[1]]);
-  }
+  for (int s2 = 0; s2 < KSUB; ++s2)
+#pragma unroll
+    for (int j = 0; j < WTN; ++j) fb[s2][j] = to_f16(*(const tbx8 *)(smem + boff[s2][j]));
+  fa[0] = *(const f16x8 *)(smem + aoff[0]);
+  fa[1] = *(const f16x8 *)(smem + aoff[1]);
 
   for (int i = 0; i < nk; ++i) {
     const int cur = i % NST, nxt = (i + 1) % NST;
-    const f16 *sA = (const f16 *)(smem + cur * STAGE_BYTES);
-    const f16 *sAn = (const f16 *)(smem + nxt * STAGE_BYTES);
-    const bf16 *sBn = (const bf16 *)(smem + nxt * STAGE_BYTES + A_BYTES);
+    const char *sc = smem + cur * STAGE_BYTES;
+    const char *sn = smem + nxt * STAGE_BYTES;
     const int knext = i + NST - 1 < nk ? i + NST - 1 : nk - 1;
 #pragma unroll
-    for (int ii = 0; ii < WTM; ++ii) {
-      if (ii + 2 < WTM) fa[ii + 2] = *(const f16x8 *)(&sA[aoff[ii + 2]]);
-      if (ii == WTM / 2) {
+    for (int f = 0; f < F; ++f) {
+      if (f + 2 < F) fa[f + 2] = *(const f16x8 *)(sc + aoff[f + 2]);
+      if (f == F / 2) {
         // stage i+1 has landed for this wave (NST-3 newer stages may be outstanding);
         // after the barrier it has landed for every wave and stage i-1 is free
         wait_vmcnt<(NST - 3) * L_DMA>();
         __builtin_amdgcn_s_barrier();
         issue(kt0 + knext, (i + NST - 1) % NST);
 #pragma unroll
-        for (int j = 0; j < WTN; ++j) rbn[j] = *(const bf16x8 *)(&sBn[boff[j]]);
+        for (int s2 = 0; s2 < KSUB; ++s2)
+#pragma unroll
+          for (int j = 0; j < WTN; ++j) rbn[s2][j] = *(const tbx8 *)(sn + boff[s2][j]);
       }
       SCHED_FENCE();
 #pragma unroll
       for (int j = 0; j < WTN; ++j)
-        acc[ii][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[ii], fb[j], acc[ii][j], 0, 0, 0);
+        acc[f % WTM][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[f], fb[f / WTM][j],
+                                                                 acc[f % WTM][j], 0, 0, 0);
       SCHED_FENCE();
-      if (ii == WTM - 2) fa[0] = *(const f16x8 *)(&sAn[aoff[0]]);
-      if (ii == WTM - 1) {
-        fa[1] = *(const f16x8 *)(&sAn[aoff[1]]);
+      if (f == F - 2) fa[0] = *(const f16x8 *)(sn + aoff[0]);
+      if (f == F - 1) {
+        fa[1] = *(const f16x8 *)(sn + aoff[1]);
 #pragma unroll
-        for (int j = 0; j < WTN; ++j) fb[j] = bf16x8_to_f16x8(rbn[j]);
+        for (int s2 = 0; s2 < KSUB; ++s2)
+#pragma unroll
+          for (int j = 0; j < WTN; ++j) fb[s2][j] = to_f16(rbn[s2][j]);
       }
     }
   }
@@ -311,16 +335,21 @@ using acespec::EPI_RESID;
 using acespec::EPI_SWIGLU;
 using acespec::EPI_F32;
 
-// Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU}.
-// Measured on MI355X against the verify-step shapes (other tilings tried: 32 x 32 MFMA
-// blocks with one wave per SIMD, 64-wide k stages, weights loaded straight to VGPRs,
-// deeper rings at one workgroup per CU; none was faster than these two).
+// Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU,
+// k per stage}.  Measured on MI355X against the verify-step shapes.  Tried and slower on
+// every shape here: ping-pong pairs of waves per SIMD (one issuing 32 x 32 MFMAs while
+// the other loads), deeper rings (5-8 stages) at one workgroup per CU, 128 x 128 tiles
+// with 64-wide k stages, and fp16 weights (which only removes the in-register widening,
+// worth 3-8 %).  The limit of the 128 x 256 tiling is the L2 -> LDS path, not the MFMA
+// pipe: with the DMA removed it runs at 1.9 PFLOP/s, with the MFMAs removed at 75 % of
+// its full time.
 struct GemmVariant {
-  int wmn, wnn, wtm, wtn, nst, occ;
+  int wmn, wnn, wtm, wtn, nst, occ, kss;
 };
 constexpr GemmVariant kVariants[] = {
-    {1, 4, 8, 4, 3, 2},  // 0: 128 x 256, wave 128 x 64, 72 KB LDS, 2 workgroups per CU
-    {2, 2, 4, 4, 4, 2},  // 1: 128 x 128, wave 64 x 64, 64 KB LDS, 2 workgroups per CU
+    {1, 4, 8, 4, 3, 2, 32},   // 0: 128 x 256, 4 waves of 128 x 64, 72 KB LDS, 2 WGs per CU
+    {2, 2, 4, 4, 4, 2, 32},   // 1: 128 x 128, 4 waves of 64 x 64, 64 KB LDS, 2 WGs per CU
+    {2, 4, 4, 4, 3, 1, 64},   // 2: 128 x 256, 8 waves of 64 x 64, k 64, 144 KB LDS, 1 WG per CU
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -341,32 +370,33 @@ int choose_splits(int epi, int M, int N, int K, int tiles, int cus, int occ) {
   return best;
 }
 
-template <int EPI, int V>
-void launch_variant(dim3 grid, hipStream_t s, const f16 *A, const bf16 *W, int M, int N, int K,
+template <int EPI, int V, typename TB>
+void launch_variant(dim3 grid, hipStream_t s, const f16 *A, const TB *W, int M, int N, int K,
                     f16 *out, float *outf, float *part, int mt, int nt, int splits) {
   constexpr GemmVariant v = kVariants[V];
-  hipLaunchKernelGGL((gemm_f16w_kernel<EPI, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ>), grid,
-                     dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
-                     splits);
+  hipLaunchKernelGGL(
+        (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>), grid,
+        dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
 }
 
-template <int EPI>
-void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const bf16 *W, int M, int N,
+template <int EPI, typename TB>
+void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const TB *W, int M, int N,
                 int K, f16 *out, float *outf, float *part, int mt, int nt, int splits) {
   switch (var) {
-#define CASE(V) case V: launch_variant<EPI, V>(grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    CASE(0) CASE(1)
+#define CASE(V) case V: launch_variant<EPI, V, TB>(grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    CASE(0) CASE(1) CASE(2)
 #undef CASE
     default: break;
   }
 }
 
 // Default tiling per shape (measured on MI355X): 128 x 128 tiles for few rows (more
-// tiles to spread over 256 CUs) and for QKV-sized fp32 outputs, 128 x 256 otherwise.
+// tiles to spread over 256 CUs), the 8-wave 64-wide-k tiling for QKV-sized fp32
+// outputs, 128 x 256 otherwise.
 int pick_variant(int epi, int M, int N, int K) {
   (void)K;
   if (M <= 384) return 1;
-  if (epi == EPI_F32 && N <= 8192) return 1;
+  if (epi == EPI_F32 && N <= 8192) return 2;
   return 0;
 }
 
@@ -374,8 +404,9 @@ int pick_variant(int epi, int M, int N, int K) {
 
 namespace acespec {
 
+template <typename TB>
 hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
-                               const bf16 *W, int M, int N, int K, f16 *out, float *outf,
+                               const TB *W, int M, int N, int K, f16 *out, float *outf,
                                float *part, long long part_cap, int cus, hipStream_t s) {
   if (var < 0) var = pick_variant(epi, M, N, K);
   if (var >= kNumVariants) return hipErrorInvalidValue;
@@ -389,10 +420,10 @@ hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 
   while (splits > 1 && (long long)splits * M * N > part_cap) --splits;
   const dim3 grid(mt * nt * splits);
   switch (epi) {
-    case EPI_STORE: launch_epi<EPI_STORE>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    case EPI_RESID: launch_epi<EPI_RESID>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    case EPI_SWIGLU: launch_epi<EPI_SWIGLU>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    default: launch_epi<EPI_F32>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
+    case EPI_STORE: launch_epi<EPI_STORE, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    case EPI_RESID: launch_epi<EPI_RESID, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+    default: launch_epi<EPI_F32, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
@@ -406,11 +437,15 @@ hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 
   return hipGetLastError();
 }
 
+template hipError_t launch_f16w_variant<bf16>(int, int, int, const f16 *, const bf16 *, int, int,
+                                              int, f16 *, float *, float *, long long, int,
+                                              hipStream_t);
+
 template <>
 hipError_t launch_gemm<bf16, f16>(int epi, const f16 *A, const bf16 *W, int M, int N, int K,
                                   f16 *out, float *outf, const GemmAux &aux, hipStream_t s) {
-  return launch_f16w_variant(-1, 0, epi, A, W, M, N, K, out, outf, aux.part, aux.part_cap,
-                             aux.cus, s);
+  return launch_f16w_variant<bf16>(-1, 0, epi, A, W, M, N, K, out, outf, aux.part,
+                                   aux.part_cap, aux.cus, s);
 }
 
 template <>
