@@ -161,6 +161,25 @@ int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final
                         const acespec_params *params, const acespec_outputs *outs,
                         hipStream_t stream);
 
+/* Commits the accepted path of every session into its KV cache (Algorithm 1, the
+ * cloud's COMPACT_KV after RECEIVE_WAIT: only the state of the kept prefix survives a
+ * verify round).  Inputs are a verify_tree call's outputs over the same cache:
+ *  path [B, N+1], path_len [B]: the kept drafted rows root-first (outs->path, path_len);
+ *  status [B] or NULL: sessions whose status is not ACESPEC_OK are not committed.
+ * For every layer and kv head, the keys and values of row 0 (the root) and of the kept
+ * rows path[b, 0 .. path_len[b]) move from slots prefix_len[b] + row to the contiguous
+ * slots prefix_len[b] + 0 .. prefix_len[b] + path_len[b] -- the slots a causal decode of
+ * the accepted tokens fills, since a kept node at depth i sits at RoPE position
+ * prefix_len[b] + i.  Slots below prefix_len[b] are not touched; the tree slots past the
+ * new end keep stale entries.
+ *  new_prefix_len [B] DEVICE output: prefix_len[b] + 1 + path_len[b], or -1 for a session
+ *  that was not committed (bad status, prefix_len + N + 1 > capacity, path_len outside
+ *  [0, N] or a kept row outside [1, N]); nothing of such a session is moved.
+ * The next round's root is the verify step's next_token (not yet in the cache). */
+int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_t *path,
+                      const int32_t *path_len, const int32_t *status, int B, int N,
+                      int32_t *new_prefix_len, hipStream_t stream);
+
 /* Message for the last non-OK return on this thread ("" if none). */
 const char *acespec_last_error(void);
 

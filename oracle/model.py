@@ -144,9 +144,11 @@ def validate_tree(parents: Sequence[int], tokens: Sequence[int], V: int) -> bool
 
 def tree_layer(W: F64Weights, dims: Dims, l: int, x: np.ndarray, kpre: np.ndarray,
                vpre: np.ndarray, cos: np.ndarray, sin: np.ndarray, anc: np.ndarray,
-               S: int) -> np.ndarray:
+               S: int, kv_sink: list = None) -> np.ndarray:
     """One decoder layer over the n rows of one tree.  kpre / vpre: [Hkv, S, hd] prefix
-    (keys post-RoPE).  Row r attends to the S prefix slots and to rows j with anc[r, j]."""
+    (keys post-RoPE).  Row r attends to the S prefix slots and to rows j with anc[r, j].
+    kv_sink, if given, receives this layer's tree-row keys (post-RoPE) and values, each
+    [n, Hkv, hd]."""
     n = x.shape[0]
     H, Hkv, hd, G = dims.H, dims.Hkv, dims.hd, dims.G
     scale = 1.0 / np.sqrt(hd)
@@ -157,6 +159,8 @@ def tree_layer(W: F64Weights, dims: Dims, l: int, x: np.ndarray, kpre: np.ndarra
     v = qkv[:, (H + Hkv) * hd:].reshape(n, Hkv, hd)
     q = apply_rope(q, cos, sin)
     k = apply_rope(k, cos, sin)
+    if kv_sink is not None:
+        kv_sink.append((k.copy(), v.copy()))
     o = np.zeros((n, H, hd))
     visible = np.concatenate([np.ones((n, S), dtype=bool), anc], axis=1)
     for h in range(H):
@@ -178,17 +182,18 @@ def final_logits(W: F64Weights, dims: Dims, x: np.ndarray) -> np.ndarray:
 
 def forward_tree_session(W: F64Weights, dims: Dims, kpre: List[np.ndarray],
                          vpre: List[np.ndarray], tokens: Sequence[int],
-                         parents: Sequence[int], S: int) -> np.ndarray:
+                         parents: Sequence[int], S: int, kv_sink: list = None) -> np.ndarray:
     """Logits z[r] (float64, [n, V]) for every row of one drafted tree.
 
     kpre / vpre: per layer, the session's cache prefix [Hkv, S, hd] (keys post-RoPE).
+    kv_sink, if given, receives per layer the tree rows' (keys, values) [n, Hkv, hd].
     """
     depth = np.array(tree_depths(parents))
     anc = ancestor_matrix(parents)
     cos, sin = rope_cos_sin(S + depth, dims.hd, dims.rope_base)
     x = W.embed_rows(tokens)
     for l in range(dims.L):
-        x = tree_layer(W, dims, l, x, kpre[l], vpre[l], cos, sin, anc, S)
+        x = tree_layer(W, dims, l, x, kpre[l], vpre[l], cos, sin, anc, S, kv_sink)
     return final_logits(W, dims, x)
 
 
@@ -199,13 +204,14 @@ def forward_tree_session(W: F64Weights, dims: Dims, kpre: List[np.ndarray],
 
 def forward_causal_path(W: F64Weights, dims: Dims, kpre: List[np.ndarray],
                         vpre: List[np.ndarray], path_tokens: Sequence[int],
-                        S: int) -> np.ndarray:
+                        S: int, return_cache: bool = False):
     """Logits at the last token of [prefix; path_tokens], decoding one token at a time.
 
     Token i of the path sits at position S + i and sees the whole prefix and the
     path tokens before it: an ordinary causal language-model pass.  The tree
     forward must reproduce, for every row, this quantity evaluated on the
-    row's root-to-node path.
+    row's root-to-node path.  With return_cache, also returns the cache this decode
+    builds: per layer, keys and values [Hkv, S + len(path_tokens), hd].
     """
     H, Hkv, hd, G = dims.H, dims.Hkv, dims.hd, dims.G
     ks = [[kpre[l][g].copy() for g in range(Hkv)] for l in range(dims.L)]
@@ -237,7 +243,26 @@ def forward_causal_path(W: F64Weights, dims: Dims, kpre: List[np.ndarray],
         if i == len(path_tokens) - 1:
             xn = rms_norm(x[None, :], W.get("final_norm"), dims.rms_eps)[0]
             logits = W.get("lm_head") @ xn
+    if return_cache:
+        return logits, ([np.stack(ks[l]) for l in range(dims.L)],
+                        [np.stack(vs[l]) for l in range(dims.L)])
     return logits
+
+
+def commit_path(k_cache: np.ndarray, v_cache: np.ndarray, S: int, path: Sequence[int]):
+    """COMPACT_KV of Algorithm 1 on one session's cache.
+
+    k_cache [L, Hkv, cap, hd] and v_cache [L, Hkv, hd, cap] (values head-dim-major, the
+    cache layout) hold the tree rows' entries at slots S + row after a verify step.  The
+    cloud keeps the root (row 0) and the accepted rows `path` (root-first) and discards
+    the rest: their entries move, in path order, to slots S, S + 1, ...  Returns the new
+    arrays and the new prefix length S + 1 + len(path)."""
+    rows = [0] + [int(r) for r in path]
+    src = [S + r for r in rows]
+    k, v = k_cache.copy(), v_cache.copy()
+    k[:, :, S: S + len(rows), :] = k_cache[:, :, src, :]
+    v[:, :, :, S: S + len(rows)] = v_cache[:, :, :, src]
+    return k, v, S + len(rows)
 
 
 def path_to(parents: Sequence[int], r: int) -> List[int]:

@@ -18,7 +18,8 @@ ACESPEC_ENOMEM, ACESPEC_EHIP, ACESPEC_EBADTREE = -3, -4, -5
 ACESPEC_F32, ACESPEC_BF16 = 0, 1
 
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree", "acespec_verify_tail",
-            "acespec_last_error", "acespec_timing_enable", "acespec_timing_read"]
+            "acespec_commit_kv", "acespec_last_error", "acespec_timing_enable",
+            "acespec_timing_read"]
 
 
 class ModelDesc(C.Structure):
@@ -81,6 +82,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int,
                                         C.POINTER(Params), C.POINTER(Outputs), C.c_void_p]
     lib.acespec_verify_tail.restype = C.c_int
+    lib.acespec_commit_kv.argtypes = [C.c_void_p, C.POINTER(KVCache), C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+    lib.acespec_commit_kv.restype = C.c_int
     lib.acespec_last_error.argtypes = []
     lib.acespec_last_error.restype = C.c_char_p
     lib.acespec_timing_enable.argtypes = [C.c_void_p, C.c_int]
@@ -137,6 +141,12 @@ def acespec_verify_tail(ctx, lm_head: int, final_norm: Optional[int], hidden: in
     return _check(load().acespec_verify_tail(ctx, lm_head, final_norm, hidden, draft_tokens,
                                              draft_q, uniforms, R, chain_len, C.byref(params),
                                              C.byref(outputs), stream))
+
+
+def acespec_commit_kv(ctx, kv: KVCache, path: int, path_len: int, status: Optional[int], B: int,
+                      N: int, new_prefix_len: int, stream: int) -> int:
+    return _check(load().acespec_commit_kv(ctx, C.byref(kv), path, path_len, status, B, N,
+                                           new_prefix_len, stream))
 
 
 def acespec_timing_enable(ctx, enable: bool) -> None:
@@ -237,6 +247,13 @@ class Verifier:
         return acespec_verify_tree(self.ctx, wstruct, kv, _ptr(tokens), _ptr(parents), _ptr(q),
                                    _ptr(u), B, n1 - 1, Params(T, top_p, k),
                                    self.outputs_struct(outs), self._stream())
+
+    def commit_kv(self, kv_k, kv_v, capacity: int, prefix_len, path, path_len, status,
+                  new_prefix_len) -> int:
+        B, n1 = path.shape
+        kv = KVCache(_ptr(kv_k), _ptr(kv_v), capacity, _ptr(prefix_len))
+        return acespec_commit_kv(self.ctx, kv, _ptr(path), _ptr(path_len), _ptr(status), B,
+                                 n1 - 1, _ptr(new_prefix_len), self._stream())
 
     def verify_tail(self, lm_head, final_norm, hidden, draft, q, u, chain_len: int, T: float,
                     top_p: float, k: int, outs: Dict) -> int:

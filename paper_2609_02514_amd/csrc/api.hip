@@ -34,12 +34,13 @@ int fail(int code, const char *fmt, ...) {
 
 enum Kind {
   K_TREE, K_EMBED, K_RMSNORM, K_GEMM_QKV, K_ROPE, K_ATTN, K_GEMM_O, K_GEMM_GATE_UP,
-  K_GEMM_DOWN, K_GEMM_LM, K_VOCAB, K_WALK, K_COUNT
+  K_GEMM_DOWN, K_GEMM_LM, K_VOCAB, K_WALK, K_COMMIT, K_COUNT
 };
 const char *kKindNames[K_COUNT] = {"tree_prep",    "embed",       "rmsnorm",
                                    "gemm_qkv",     "rope_kv",     "tree_attention",
                                    "gemm_o",       "gemm_gate_up", "gemm_down",
-                                   "gemm_lm_head", "vocab_verify", "path_walk"};
+                                   "gemm_lm_head", "vocab_verify", "path_walk",
+                                   "commit_kv"};
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -432,6 +433,32 @@ int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final
                                   uniforms, R, chain_len, p, o, stream);
   return verify_tail_impl<float>(ctx, lm_head, final_norm, hidden, draft_tokens, draft_q,
                                  uniforms, R, chain_len, p, o, stream);
+}
+
+int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_t *path,
+                      const int32_t *path_len, const int32_t *status, int B, int N,
+                      int32_t *new_prefix_len, hipStream_t stream) {
+  g_err.clear();
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  if (ctx->d.n_layers < 1) return fail(ACESPEC_EINVAL, "the model has no layers (no KV cache)");
+  if (!kv || !kv->k || !kv->v || !kv->prefix_len || !path || !path_len || !new_prefix_len)
+    return fail(ACESPEC_EINVAL, "a required pointer is NULL (only status may be)");
+  if (B < 1 || B > ctx->max_batch)
+    return fail(ACESPEC_EINVAL, "B must be in [1, %d] (got %d)", ctx->max_batch, B);
+  if (N < 0 || N > ctx->max_nodes)
+    return fail(ACESPEC_EINVAL, "N must be in [0, %d] (got %d)", ctx->max_nodes, N);
+  if (kv->capacity < N + 1)
+    return fail(ACESPEC_EINVAL, "kv capacity %d cannot hold the %d tree rows", kv->capacity, N + 1);
+  const acespec_model_desc &d = ctx->d;
+  if (d.dtype == ACESPEC_BF16)
+    RUN(K_COMMIT, launch_commit_kv<bf16>((bf16 *)kv->k, (bf16 *)kv->v, kv->prefix_len, path,
+                                         path_len, status, d.n_layers, B, N + 1, d.n_kv_heads,
+                                         d.head_dim, kv->capacity, new_prefix_len, stream));
+  else
+    RUN(K_COMMIT, launch_commit_kv<float>((float *)kv->k, (float *)kv->v, kv->prefix_len, path,
+                                          path_len, status, d.n_layers, B, N + 1, d.n_kv_heads,
+                                          d.head_dim, kv->capacity, new_prefix_len, stream));
+  return ACESPEC_OK;
 }
 
 int acespec_timing_enable(acespec_ctx *ctx, int enable) {

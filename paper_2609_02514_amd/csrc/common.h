@@ -201,6 +201,15 @@ hipError_t launch_walk(const int32_t *tok, const int32_t *par, const uint8_t *ac
                        int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
                        int32_t *next_token, uint8_t *sibling_hit, hipStream_t s);
 
+// Algorithm 1 COMPACT_KV: moves the root and kept rows of each session to the slots
+// following its prefix; new_len[b] = prefix_len[b] + 1 + path_len[b], or -1 (nothing moved)
+// if the session's status or path data is not valid.
+template <typename T>
+hipError_t launch_commit_kv(T *ck, T *cv, const int32_t *prefix_len, const int32_t *path,
+                            const int32_t *path_len, const int32_t *status, int L, int B,
+                            int n1, int Hkv, int hd, int capacity, int32_t *new_len,
+                            hipStream_t s);
+
 hipError_t launch_walk_tail(const uint8_t *accept, const int32_t *resample,
                             const int32_t *draft, int R, int chain_len, int V,
                             int32_t *acc_prefix_len, int32_t *path,

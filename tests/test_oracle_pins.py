@@ -453,3 +453,59 @@ def test_workload_tree_shapes(name, N, P):
     assert sum(1 for c in ch if c) == P
     depths = om.tree_depths(parents)
     assert max(depths) == w.depth
+
+
+# ---------------------------------------------------------------------------------------
+# KV commit (Algorithm 1, COMPACT_KV)
+# ---------------------------------------------------------------------------------------
+
+
+def test_commit_hand_vector():
+    """Entries are labelled by their slot; path [2, 4] keeps slots S+0, S+2, S+4 and moves
+    them to S, S+1, S+2 (Algorithm 1: the cloud keeps the accepted prefix only)."""
+    cap, S = 8, 2
+    k = np.zeros((1, 1, cap, 2))
+    v = np.zeros((1, 1, 2, cap))
+    for s in range(cap):
+        k[0, 0, s] = [s, 10 + s]
+        v[0, 0, :, s] = [100 + s, 200 + s]
+    k2, v2, n = om.commit_path(k, v, S, [2, 4])
+    assert n == 5
+    assert k2[0, 0, :, 0].tolist() == [0, 1, 2, 4, 6, 5, 6, 7]
+    assert k2[0, 0, :, 1].tolist() == [10, 11, 12, 14, 16, 15, 16, 17]
+    assert v2[0, 0, 0].tolist() == [100, 101, 102, 104, 106, 105, 106, 107]
+    assert v2[0, 0, 1].tolist() == [200, 201, 202, 204, 206, 205, 206, 207]
+    k3, v3, n3 = om.commit_path(k, v, S, [])        # nothing accepted: the root stays
+    assert n3 == S + 1 and np.array_equal(k3, k) and np.array_equal(v3, v)
+
+
+@pytest.mark.parametrize("path", [[1, 3, 5], [2], [1, 4], []])
+def test_commit_equals_causal_decode_cache(path):
+    """After a tree verify pass and the commit of a kept path, the cache equals the one a
+    plain causal decode of [prefix; root, kept tokens] builds (positions S + depth)."""
+    w = tiny_workload(tree="chain_sib", depth=3, sib=1, tokens="draft")
+    W, batch, S, kp, vp, toks, pars = _session(w, b=0)
+    # the kept rows must form a root-first chain of the tree
+    for a, b_ in zip([0] + path, path):
+        assert pars[b_] == a
+    dims = om.dims_of(w)
+    F = om.F64Weights(W)
+    sink = []
+    om.forward_tree_session(F, dims, kp, vp, toks, pars, S, kv_sink=sink)
+    n1, cap = len(toks), S + len(toks) + 3
+    kc = np.full((w.L, w.Hkv, cap, w.hd), np.nan)
+    vc = np.full((w.L, w.Hkv, w.hd, cap), np.nan)
+    for l in range(w.L):
+        kc[l, :, :S] = kp[l]
+        vc[l, :, :, :S] = vp[l].transpose(0, 2, 1)
+        kt, vt = sink[l]                                   # [n1, Hkv, hd]
+        kc[l, :, S:S + n1] = kt.transpose(1, 0, 2)
+        vc[l, :, :, S:S + n1] = vt.transpose(1, 2, 0)
+    k2, v2, n = om.commit_path(kc, vc, S, path)
+    assert n == S + 1 + len(path)
+    _, (kref, vref) = om.forward_causal_path(F, dims, kp, vp, [toks[r] for r in [0] + path], S,
+                                             return_cache=True)
+    for l in range(w.L):
+        np.testing.assert_allclose(k2[l, :, :n], kref[l], rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(v2[l, :, :, :n], vref[l].transpose(0, 2, 1), rtol=1e-12,
+                                   atol=1e-12)
