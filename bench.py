@@ -299,6 +299,25 @@ def main():
     roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["algorithmic_per_launch"] = {"flops": work[dom][0], "bytes": work[dom][1]} if dom in work else None
 
+    # The commit that follows a verify round (Algorithm 1, COMPACT_KV), timed on its own
+    # over the kept paths of the last verify step.
+    commit = None
+    if w.L > 0:
+        new_len = torch.empty(B, dtype=torch.int32, device="cuda")
+        acespec_timing_enable(v.ctx, True)
+        acespec_timing_read(v.ctx)
+        for _ in range(args.steps):
+            v.commit_kv(batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, outs["path"],
+                        outs["path_len"], outs["status"], new_len)
+        ck = acespec_timing_read(v.ctx).get("commit_kv")
+        acespec_timing_enable(v.ctx, False)
+        kept = int(outs["path_len"].sum().item())
+        moved = 2 * 2 * kept * w.L * w.Hkv * w.hd * 2   # K and V, read + write, bf16
+        if ck:
+            avg = ck[0] / max(ck[1], 1)
+            commit = {"avg_launch_ms": round(avg, 5), "kept_rows": kept,
+                      "algorithmic_bytes": moved, "gbs": round(moved / (avg / 1e3) / 1e9, 1)}
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host (bounded sample)")
@@ -325,6 +344,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "commit_kv": commit,
     }
     print(json.dumps(line), flush=True)
     v.close()

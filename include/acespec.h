@@ -144,6 +144,25 @@ int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *weights,
                         const float *uniforms, int B, int N, const acespec_params *params,
                         const acespec_outputs *outs, hipStream_t stream);
 
+/* The same step for the paper's own uplink (Section III-B: the edge sends the drafted
+ * tokens and a compressed draft distribution, Algorithm 1 line 3; the cloud "skips token
+ * resampling" and returns the rejection index with a sparse target distribution):
+ *  q_hat [B, N+1] fp32: q_hat[b, r] = the draft probability of row r's own token under
+ *                its parent's draft distribution (row 0 unused) -- one float per node
+ *                instead of a vocabulary-sized row.
+ * Per row: accept (u[.., 0] * q_hat < p), acc_prefix_len, topk_ids / topk_probs as in
+ * acespec_verify_tree; resample_token = bonus_token = -1 (no cloud-side sampling).
+ * Per session: path / path_len along accepted main children (no sibling hits: they need
+ * the resample token), next_token = -1, sibling_hit = 0.  The edge resamples from the
+ * top-k payload of row path_len (acc. position) against its own draft distribution;
+ * that is exact only where the payload covers the target's nucleus. */
+int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *weights,
+                                 const acespec_kv_cache *kv, const int32_t *tree_tokens,
+                                 const int32_t *parent_idx, const float *q_hat,
+                                 const float *uniforms, int B, int N,
+                                 const acespec_params *params, const acespec_outputs *outs,
+                                 hipStream_t stream);
+
 /* LM head and verification only, over R given hidden states (the last stage of
  * verify_tree on its own).  Each row r is the parent of one drafted token
  * draft_tokens[r]; rows form chains of chain_len consecutive rows (R % chain_len == 0).

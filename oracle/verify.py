@@ -224,3 +224,41 @@ def walk_tail(accept: np.ndarray, resample: np.ndarray, chain_len: int):
         path_len[b] = i
         nxt[b] = resample[b * chain_len + i] if i < chain_len else -1
     return path_len, nxt
+
+
+# ---------------------------------------------------------------------------------------
+# The paper's own protocol: scalar q-hat uplink, sparse downlink, edge-side resampling
+# ---------------------------------------------------------------------------------------
+
+
+def accept_scalar(p: np.ndarray, x: int, q_hat: float, u0: float) -> bool:
+    """Acceptance of a drafted token from its draft probability alone (the uplink carries
+    q(x) per drafted token, Algorithm 1 line 3): accept iff u0 * q_hat < p(x)."""
+    return bool(u0 * q_hat < p[x])
+
+
+def edge_resample(ids, probs, q: np.ndarray, u: float, rejected: bool = True) -> int:
+    """RESAMPLE(P_hat, Q) of Algorithm 1 on the edge, from the cloud's k-sparse payload.
+
+    After a rejection the corrected token follows max(0, P_hat - Q) over the payload's ids
+    (P_hat if that is all zero); after full acceptance it follows P_hat.  Inverse CDF in
+    ascending id order, first running mass strictly above u times the total."""
+    pairs = sorted(zip([int(i) for i in ids], [float(p) for p in probs]))
+    weights = []
+    for i, p in pairs:
+        weights.append(max(p - float(q[i]), 0.0) if rejected else p)
+    if sum(weights) <= 0.0:
+        weights = [p for _, p in pairs]
+    total = sum(weights)
+    run = 0.0
+    for (i, _), w in zip(pairs, weights):
+        run += w
+        if w > 0.0 and run > u * total:
+            return i
+    return [i for (i, _), w in zip(pairs, weights) if w > 0.0][-1]
+
+
+def exact_residual_law(p: np.ndarray, q: np.ndarray) -> np.ndarray:
+    """The law of the exact residual resample over the whole vocabulary."""
+    r = np.maximum(p - q, 0.0)
+    return r / r.sum() if r.sum() > 0 else p / p.sum()

@@ -17,9 +17,9 @@ ACESPEC_OK, ACESPEC_EINVAL, ACESPEC_EUNSUPPORTED = 0, -1, -2
 ACESPEC_ENOMEM, ACESPEC_EHIP, ACESPEC_EBADTREE = -3, -4, -5
 ACESPEC_F32, ACESPEC_BF16 = 0, 1
 
-EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree", "acespec_verify_tail",
-            "acespec_commit_kv", "acespec_last_error", "acespec_timing_enable",
-            "acespec_timing_read"]
+EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",
+            "acespec_verify_tree_scalar_q", "acespec_verify_tail", "acespec_commit_kv",
+            "acespec_last_error", "acespec_timing_enable", "acespec_timing_read"]
 
 
 class ModelDesc(C.Structure):
@@ -78,6 +78,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
                                         C.c_int, C.c_int, C.POINTER(Params),
                                         C.POINTER(Outputs), C.c_void_p]
     lib.acespec_verify_tree.restype = C.c_int
+    lib.acespec_verify_tree_scalar_q.argtypes = lib.acespec_verify_tree.argtypes
+    lib.acespec_verify_tree_scalar_q.restype = C.c_int
     lib.acespec_verify_tail.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int,
                                         C.POINTER(Params), C.POINTER(Outputs), C.c_void_p]
@@ -133,6 +135,15 @@ def acespec_verify_tree(ctx, weights: Weights, kv: KVCache, tree_tokens: int, pa
     return _check(load().acespec_verify_tree(ctx, C.byref(weights), C.byref(kv), tree_tokens,
                                              parent_idx, draft_q, uniforms, B, N,
                                              C.byref(params), C.byref(outputs), stream))
+
+
+def acespec_verify_tree_scalar_q(ctx, weights: Weights, kv: KVCache, tree_tokens: int,
+                                 parent_idx: int, q_hat: int, uniforms: int, B: int, N: int,
+                                 params: Params, outputs: Outputs, stream: int) -> int:
+    return _check(load().acespec_verify_tree_scalar_q(ctx, C.byref(weights), C.byref(kv),
+                                                      tree_tokens, parent_idx, q_hat, uniforms,
+                                                      B, N, C.byref(params), C.byref(outputs),
+                                                      stream))
 
 
 def acespec_verify_tail(ctx, lm_head: int, final_norm: Optional[int], hidden: int,
@@ -247,6 +258,15 @@ class Verifier:
         return acespec_verify_tree(self.ctx, wstruct, kv, _ptr(tokens), _ptr(parents), _ptr(q),
                                    _ptr(u), B, n1 - 1, Params(T, top_p, k),
                                    self.outputs_struct(outs), self._stream())
+
+    def verify_tree_scalar_q(self, wstruct: Weights, kv_k, kv_v, capacity: int, prefix_len,
+                             tokens, parents, q_hat, u, T: float, top_p: float, k: int,
+                             outs: Dict) -> int:
+        B, n1 = tokens.shape
+        kv = KVCache(_ptr(kv_k), _ptr(kv_v), capacity, _ptr(prefix_len))
+        return acespec_verify_tree_scalar_q(self.ctx, wstruct, kv, _ptr(tokens), _ptr(parents),
+                                            _ptr(q_hat), _ptr(u), B, n1 - 1, Params(T, top_p, k),
+                                            self.outputs_struct(outs), self._stream())
 
     def commit_kv(self, kv_k, kv_v, capacity: int, prefix_len, path, path_len, status,
                   new_prefix_len) -> int:

@@ -131,8 +131,8 @@ int check_outputs(const acespec_outputs *o) {
 template <typename T>
 int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
                      const int32_t *tokens, const int32_t *parents, const float *draft_q,
-                     const float *uniforms, int B, int N, const acespec_params *p,
-                     const acespec_outputs *o, hipStream_t stream) {
+                     const float *q_scalar, const float *uniforms, int B, int N,
+                     const acespec_params *p, const acespec_outputs *o, hipStream_t stream) {
   typedef typename ActOf<T>::type A;
   const acespec_model_desc &d = ctx->d;
   const int n1 = N + 1, R = B * n1;
@@ -178,6 +178,7 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   VocabArgs va;
   va.logits = logits;
   va.q = draft_q;
+  va.q_scalar = q_scalar;
   va.u = uniforms;
   va.tok = meta.tok;
   va.par = meta.par;
@@ -227,6 +228,7 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   VocabArgs va;
   va.logits = logits;
   va.q = draft_q;
+  va.q_scalar = nullptr;
   va.u = uniforms;
   va.tok = draft;
   va.par = nullptr;
@@ -372,16 +374,22 @@ void acespec_destroy(acespec_ctx *c) {
   delete c;
 }
 
-int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
+}  // extern "C"
+
+namespace {
+
+// Shared argument checks and dispatch of the two verify_tree entry points (dense draft
+// distributions, or the scalar q-hat of each drafted token).
+int verify_tree_checked(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
                         const int32_t *tree_tokens, const int32_t *parent_idx,
-                        const float *draft_q, const float *uniforms, int B, int N,
-                        const acespec_params *p, const acespec_outputs *o,
+                        const float *draft_q, const float *q_scalar, const float *uniforms,
+                        int B, int N, const acespec_params *p, const acespec_outputs *o,
                         hipStream_t stream) {
   g_err.clear();
   if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
   const acespec_model_desc &d = ctx->d;
   if (d.n_layers < 1) return fail(ACESPEC_EINVAL, "context has no layers (tail-only model)");
-  if (!w || !kv || !tree_tokens || !parent_idx || !draft_q || !uniforms)
+  if (!w || !kv || !tree_tokens || !parent_idx || !(draft_q || q_scalar) || !uniforms)
     return fail(ACESPEC_EINVAL, "a required pointer is NULL");
   if (!w->embed || !w->layers || !w->final_norm || !w->lm_head)
     return fail(ACESPEC_EINVAL, "a weight pointer is NULL");
@@ -405,10 +413,40 @@ int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespe
   rc = check_outputs(o);
   if (rc) return rc;
   if (d.dtype == ACESPEC_BF16)
-    return verify_tree_impl<bf16>(ctx, w, kv, tree_tokens, parent_idx, draft_q, uniforms, B, N,
-                                  p, o, stream);
-  return verify_tree_impl<float>(ctx, w, kv, tree_tokens, parent_idx, draft_q, uniforms, B, N,
-                                 p, o, stream);
+    return verify_tree_impl<bf16>(ctx, w, kv, tree_tokens, parent_idx, draft_q, q_scalar,
+                                  uniforms, B, N, p, o, stream);
+  return verify_tree_impl<float>(ctx, w, kv, tree_tokens, parent_idx, draft_q, q_scalar,
+                                 uniforms, B, N, p, o, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
+                        const int32_t *tree_tokens, const int32_t *parent_idx,
+                        const float *draft_q, const float *uniforms, int B, int N,
+                        const acespec_params *p, const acespec_outputs *o,
+                        hipStream_t stream) {
+  if (!draft_q) {
+    g_err.clear();
+    return fail(ACESPEC_EINVAL, "draft_q is NULL");
+  }
+  return verify_tree_checked(ctx, w, kv, tree_tokens, parent_idx, draft_q, nullptr, uniforms, B,
+                             N, p, o, stream);
+}
+
+int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *w,
+                                 const acespec_kv_cache *kv, const int32_t *tree_tokens,
+                                 const int32_t *parent_idx, const float *q_hat,
+                                 const float *uniforms, int B, int N, const acespec_params *p,
+                                 const acespec_outputs *o, hipStream_t stream) {
+  if (!q_hat) {
+    g_err.clear();
+    return fail(ACESPEC_EINVAL, "q_hat is NULL");
+  }
+  return verify_tree_checked(ctx, w, kv, tree_tokens, parent_idx, nullptr, q_hat, uniforms, B,
+                             N, p, o, stream);
 }
 
 int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,

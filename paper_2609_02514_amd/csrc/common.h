@@ -180,7 +180,8 @@ hipError_t launch_attention(const typename ActOf<TW>::type *q, const TW *cache_k
 
 struct VocabArgs {
   const float *logits;      // [rows, V]
-  const float *q;           // [rows, V]
+  const float *q;           // [rows, V] dense draft distributions (NULL in scalar mode)
+  const float *q_scalar;    // [rows] q-hat of each row's own token, or NULL (dense mode)
   const float *u;           // [rows, 3]
   const int32_t *tok;       // [rows] token of each row (children look theirs up here)
   const int32_t *par;       // [rows] parent row within the session, -1 for the root

@@ -432,7 +432,12 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   if (!tail) {
     for (int c = r + 1; c < a.n1; ++c) has_child |= a.par[srow0 + c] == r;
   }
-  const float *q = a.q + (size_t)row * V;
+  // Scalar mode: the uplink carries only q-hat of each drafted token (one float per
+  // child row); the cloud then tests acceptance and does no sampling, so the residual
+  // mass (the only reader of a dense q row) is not needed.
+  const bool dense_q = a.q_scalar == nullptr;
+  const bool resid = has_child && dense_q;
+  const float *q = dense_q ? a.q + (size_t)row * V : nullptr;
   for (int s = wave; s < nseg; s += NWV) {
     const int id0 = s * SEG + lane * 4;
     const bool valid = id0 < V;
@@ -440,7 +445,7 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     float4 q4 = make_float4(0.f, 0.f, 0.f, 0.f);
     if (valid) {
       z4 = *(const float4 *)(z + id0);
-      if (has_child) q4 = *(const float4 *)(q + id0);
+      if (resid) q4 = *(const float4 *)(q + id0);
     }
     const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
     const float qq[4] = {q4.x, q4.y, q4.z, q4.w};
@@ -464,7 +469,7 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
       const bool inn = in_nucleus(key[j], rp[j], sel);
       const float p = elem_p(zz[j], inn, sel);
       sp_ += fixw(p);
-      if (has_child) sr_ += fixw(fmaxf(p - qq[j], 0.f));
+      if (resid) sr_ += fixw(fmaxf(p - qq[j], 0.f));
       if (in_topk(key[j], rk[j], sel)) {
         const uint32_t slot = atomicAdd(&sm.ncand, 1u);
         if (slot < KMAX) {
@@ -520,9 +525,12 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   // ---- bonus sample from p_r --------------------------------------------------------------
   const float *u = a.u;
   if (wave == 0) {
-    const u64 target = (u64)floor((double)u[(size_t)row * 3 + 2] * (double)Ptot);
-    const int sg = find_segment(sm.seg_p, nseg, target);
-    const int id = seg_inverse_cdf(z, q, V, sg, sm.seg_p[sg], target, 0, sel, sm);
+    int id = -1;
+    if (dense_q) {
+      const u64 target = (u64)floor((double)u[(size_t)row * 3 + 2] * (double)Ptot);
+      const int sg = find_segment(sm.seg_p, nseg, target);
+      id = seg_inverse_cdf(z, q, V, sg, sm.seg_p[sg], target, 0, sel, sm);
+    }
     if (lane == 0) a.bonus[row] = id;
   }
 
@@ -566,11 +574,13 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
         rx = __shfl(mine_rank, src);
       }
       const float px = elem_p(zx, in_nucleus(kx, rx, sel), sel);
-      const float qx = q[x];
+      const float qx = dense_q ? q[x] : a.q_scalar[child];
       const float u0 = u[(size_t)child * 3 + 0], u1 = u[(size_t)child * 3 + 1];
       const bool acc = u0 * qx < px;
-      int res;
-      if (Rtot > 0) {
+      int res = -1;
+      if (!dense_q) {
+        // no cloud-side resampling in the scalar protocol
+      } else if (Rtot > 0) {
         const u64 target = (u64)floor((double)u1 * (double)Rtot);
         const int sg = find_segment(sm.seg_r, nseg, target);
         res = seg_inverse_cdf(z, q, V, sg, sm.seg_r[sg], target, 1, sel, sm);

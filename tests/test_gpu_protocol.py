@@ -1,0 +1,79 @@
+"""GPU parity of the paper's own protocol (scalar q-hat uplink, no cloud-side sampling,
+edge-side resampling from the k-sparse payload; Section III-B, Algorithm 1 lines 3-7)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import verify as ov
+from paper_2609_02514_amd import edge
+from tests import harness as hz
+from tests.test_gpu_parity import small_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def test_scalar_q_decisions_and_edge_resample():
+    from paper_2609_02514_amd.acespec import Verifier
+    w = small_bf16(B=6, ragged=True)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda")
+    B, n1 = batch.tokens.shape
+    par = batch.parents.long().clamp(min=0)
+    tok = batch.tokens.long()
+    # q_hat[b, r] = draft probability of row r's token under its parent's distribution
+    qpar = batch.q[torch.arange(B, device="cuda")[:, None], par]          # [B, n1, V]
+    q_hat = qpar.gather(2, tok.unsqueeze(-1)).squeeze(-1).contiguous()
+    q_hat[:, 0] = 0.0
+    v = Verifier.for_workload(w)
+    ws = v.weights_struct(W)
+    od = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", True)
+    osq = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", True)
+    hz.log(f"dense and scalar-q verify B={B} N={n1 - 1}")
+    v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
+                  batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, od)
+    v.verify_tree_scalar_q(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len,
+                           batch.tokens, batch.parents, q_hat, batch.u, w.T, w.top_p, w.top_k,
+                           osq)
+    torch.cuda.synchronize()
+    gd = {k: hz.host(t) for k, t in od.items()}
+    gs = {k: hz.host(t) for k, t in osq.items()}
+    v.close()
+    # the same logits, so the same accept bits (q_hat is the dense row's own float) and payload
+    for k in ("logits_out", "accept", "acc_prefix_len", "topk_ids", "topk_probs", "status"):
+        assert torch.equal(gd[k], gs[k]), k
+    assert (gs["resample_token"] == -1).all() and (gs["bonus_token"] == -1).all()
+    assert (gs["next_token"] == -1).all() and (gs["sibling_hit"] == 0).all()
+    q_h, u_h = hz.host(batch.q), hz.host(batch.u)
+    tvs = []
+    for b in range(B):
+        toks = batch.tokens[b].tolist()
+        pars = batch.parents[b].tolist()
+        res = ov.RowResult(accept=gs["accept"][b * n1:(b + 1) * n1].numpy(), acc_prefix_len=None,
+                           resample=gs["resample_token"][b * n1:(b + 1) * n1].numpy(),
+                           bonus=gs["bonus_token"][b * n1:(b + 1) * n1].numpy(), topk_ids=None,
+                           topk_probs=None, nucleus_size=None)
+        wr = ov.walk(toks, pars, res)
+        assert int(gs["path_len"][b]) == len(wr.path) and not wr.sibling_hit
+        assert gs["path"][b].tolist()[:len(wr.path)] == wr.path
+        # edge: resample at the row where the walk stopped
+        cur = wr.path[-1] if wr.path else 0
+        kids = ov.children_of(pars)[cur]
+        rejected = bool(kids)
+        u = float(u_h[b, kids[0], 1]) if rejected else float(u_h[b, cur, 2])
+        row = b * n1 + cur
+        ids, probs = gs["topk_ids"][row].numpy(), gs["topk_probs"][row].numpy()
+        qrow = q_h[b, cur].numpy().astype(np.float64)
+        t_edge = edge.resample(ids, probs, qrow, u, rejected)
+        assert t_edge == ov.edge_resample(ids, probs.astype(np.float64), qrow, u, rejected)
+        # gap to the exact residual (informational; zero when the payload covers the nucleus)
+        pt = ov.tempered_softmax(gs["logits_out"][row].numpy().astype(np.float64), w.T)
+        p, _, _ = ov.nucleus(pt, w.top_p)
+        exact = ov.exact_residual_law(p, qrow) if rejected else p / p.sum()
+        sid, sw = edge.residual_law(ids, probs, qrow, rejected)
+        sparse = np.zeros_like(exact)
+        sparse[sid] = sw
+        tvs.append(0.5 * np.abs(sparse - exact).sum())
+    hz.log(f"edge resample vs exact residual: total variation mean {np.mean(tvs):.3f} "
+           f"max {np.max(tvs):.3f} (top-k {w.top_k} of vocab {w.V})")
+    assert all(0.0 <= t <= 1.0 + 1e-9 for t in tvs)
