@@ -325,7 +325,8 @@ def main():
         log(f"oracle: {cpu['value']:.3f} tok/s on {cpu['cores']} threads")
 
     line = {
-        "metric": "verified tree tokens/s on 1 MI355X (8B shape)",
+        "metric": ("verified tree tokens/s on 1 MI355X (8B shape)" if w.name == "8b-bf16"
+                   else f"verified tree tokens/s on 1 MI355X ({w.name})"),
         "value": round(value, 1),
         "unit": "verified tree tokens/s",
         "n_gpus": 1,

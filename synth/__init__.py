@@ -104,6 +104,15 @@ WORKLOADS = {
     "8b-lmhead-tail": Workload("8b-lmhead-tail", "bf16", L=0, d=4096, H=0, Hkv=1, hd=0, F=0,
                                V=128256, B=256, S=0, tree="tail", T=0.6, top_p=0.8, top_k=8,
                                chain_len=16, rows=4096, seed_base=1239),
+    # The paper's cloud targets (Section V-A: Qwen-32B and LLaMA-70B classes) at the batch
+    # and tree shape of the 8B workload; the 70B weights (140 GB bf16) and KV cache (89 GB)
+    # fit one 288 GB GPU.
+    "32b-bf16": Workload("32b-bf16", "bf16", L=64, d=5120, H=40, Hkv=8, hd=128, F=27648,
+                         V=152064, B=64, S=2048, tree="widths_2455", depth=4, q_std=3.0,
+                         q_T=0.8, T=0.8, top_p=0.9, top_k=32, seed_base=1240),
+    "70b-bf16": Workload("70b-bf16", "bf16", L=80, d=8192, H=64, Hkv=8, hd=128, F=28672,
+                         V=128256, B=64, S=2048, tree="widths_2455", depth=4, q_std=3.0,
+                         q_T=0.8, T=0.8, top_p=0.9, top_k=32, seed_base=1241),
 }
 
 

@@ -92,6 +92,18 @@ def test_tree_8b_long_wide_sampled_session():
     _check_tree(run, tol=2e-2)
 
 
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["32b-bf16", "70b-bf16"])
+def test_tree_paper_scale_widths(name):
+    """The paper's cloud-target shapes (Qwen-32B / LLaMA-70B classes: d 5120 / 8192, G 5 / 8,
+    vocab 152064 / 128256) at their full widths and batch, two layers deep: every kernel
+    runs the launch configuration of the full-depth model (depth changes only the layer
+    loop), and the float64 oracle stays within seconds per session."""
+    w = synth.get(name).scaled(L=2)
+    run = hz.run_tree(w, sessions=[11])
+    _check_tree(run, tol=2e-2)
+
+
 # ---------------------------------------------------------------------------------------
 # LM-head tail
 # ---------------------------------------------------------------------------------------

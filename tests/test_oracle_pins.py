@@ -444,7 +444,8 @@ def test_synth_determinism_and_shapes():
 
 
 @pytest.mark.parametrize("name,N,P", [("tiny-fp32", 8, 4), ("1b-bf16", 16, 8),
-                                      ("8b-bf16", 16, 11), ("8b-long-wide", 64, 8)])
+                                      ("8b-bf16", 16, 11), ("8b-long-wide", 64, 8),
+                                      ("32b-bf16", 16, 11), ("70b-bf16", 16, 11)])
 def test_workload_tree_shapes(name, N, P):
     w = synth.get(name)
     parents = synth.tree_parents(w)
