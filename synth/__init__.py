@@ -74,6 +74,7 @@ class Workload:
     ragged: bool = False   # per-session prefix lengths in [S/2, S]
     random_gains: bool = False
     seed_base: int = 0
+    fanout: tuple = ()     # "fanout" trees: alternatives per rejection depth (F_0, F_1, ...)
 
     @property
     def N(self) -> int:
@@ -104,6 +105,13 @@ WORKLOADS = {
     "8b-lmhead-tail": Workload("8b-lmhead-tail", "bf16", L=0, d=4096, H=0, Hkv=1, hd=0, F=0,
                                V=128256, B=256, S=0, tree="tail", T=0.6, top_p=0.8, top_k=8,
                                chain_len=16, rows=4096, seed_base=1239),
+    # The 8B model with a paper-shaped tree: budget B* = 32 nodes, a main chain of 8 and
+    # B_alloc = 24 alternatives spread by the geometric decay of Section IV (alpha 0.8,
+    # beta 1), rounded by largest remainders.
+    "8b-geometric": Workload("8b-geometric", "bf16", L=32, d=4096, H=32, Hkv=8, hd=128,
+                             F=14336, V=128256, B=64, S=2048, tree="fanout", depth=8,
+                             fanout=(4, 4, 3, 3, 3, 3, 2, 2), q_std=3.0, q_T=0.8, T=0.8,
+                             top_p=0.9, top_k=32, seed_base=1242),
     # The paper's cloud targets (Section V-A: Qwen-32B and LLaMA-70B classes) at the batch
     # and tree shape of the 8B workload; the 70B weights (140 GB bf16) and KV cache (89 GB)
     # fit one 288 GB GPU.
@@ -168,6 +176,16 @@ def tree_parents(w: Workload) -> List[int]:
         return parents
     if w.tree == "chain":
         return [-1] + list(range(w.depth))
+    if w.tree == "fanout":
+        # main chain of len(fanout) nodes; at each depth k+1 the main child comes first,
+        # then fanout[k] alternative leaves under the same parent (Section III-C)
+        parents = [-1]
+        main_prev = 0
+        for fk in w.fanout:
+            main_row = len(parents)
+            parents.extend([main_prev] * (1 + fk))
+            main_prev = main_row
+        return parents
     raise ValueError(w.tree)
 
 

@@ -86,6 +86,15 @@ def test_tree_8b_full_size_sampled_session():
 
 
 @pytest.mark.timeout(900)
+def test_tree_8b_geometric_tree_sampled_session():
+    """A paper-shaped tree: main chain of 8 with 24 alternatives allocated by the geometric
+    decay of Section IV (32 drafted nodes per session)."""
+    w = synth.get("8b-geometric")
+    run = hz.run_tree(w, sessions=[23])
+    _check_tree(run, tol=2e-2)
+
+
+@pytest.mark.timeout(900)
 def test_tree_8b_long_wide_sampled_session():
     w = synth.get("8b-long-wide")
     run = hz.run_tree(w, sessions=[5])
