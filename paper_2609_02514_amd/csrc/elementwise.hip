@@ -21,38 +21,78 @@ __global__ void embed_kernel(const T *__restrict__ embed, const int32_t *__restr
   for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = to_f32(src[i]);
 }
 
-// One 256-thread block per row; d is a multiple of 64.
+// Four consecutive elements as float4 (the row bases are 16-byte aligned: d % 64 == 0).
+AS_DEVICE float4 load4(const float *p, int c) { return *(const float4 *)(p + 4 * c); }
+AS_DEVICE float4 load4(const bf16 *p, int c) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 v = *(const bf16x4 *)(p + 4 * c);
+  return make_float4((float)v[0], (float)v[1], (float)v[2], (float)v[3]);
+}
+AS_DEVICE void store4(float *p, int c, float4 v) { *(float4 *)(p + 4 * c) = v; }
+AS_DEVICE void store4(f16 *p, int c, float4 v) {
+  typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+  *(f16x4 *)(p + 4 * c) = f16x4{(f16)v.x, (f16)v.y, (f16)v.z, (f16)v.w};
+}
+
+// One 256-thread block per row; d is a multiple of 64.  A row of up to 8192 values is read
+// once (float4 per thread and step, kept in registers), longer rows are read twice.
 template <typename Tin, typename TG, typename Tout>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const Tin *__restrict__ x,
                                                       const TG *__restrict__ gain,
                                                       Tout *__restrict__ out, int d, float eps) {
-  const int row = blockIdx.x;
+  constexpr int MAXJ = 8;
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int d4 = d >> 2;
   const Tin *xr = x + (size_t)row * d;
+  float4 v[MAXJ];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = to_f32(xr[i]);
-    ss += v * v;
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    const int c = tid + 256 * j;
+    if (c < d4) {
+      v[j] = load4(xr, c);
+      ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
+    }
+  }
+  for (int c = tid + 256 * MAXJ; c < d4; c += 256) {
+    const float4 t = load4(xr, c);
+    ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
   }
   __shared__ float red[4];
   ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float scale = 1.0f / sqrtf(tot / (float)d + eps);
   Tout *o = out + (size_t)row * d;
-  for (int i = threadIdx.x; i < d; i += 256)
-    o[i] = from_f32<Tout>(to_f32(xr[i]) * scale * to_f32(gain[i]));
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    const int c = tid + 256 * j;
+    if (c < d4) {
+      const float4 g = load4(gain, c);
+      store4(o, c, make_float4(v[j].x * scale * g.x, v[j].y * scale * g.y,
+                               v[j].z * scale * g.z, v[j].w * scale * g.w));
+    }
+  }
+  for (int c = tid + 256 * MAXJ; c < d4; c += 256) {
+    const float4 t = load4(xr, c), g = load4(gain, c);
+    store4(o, c, make_float4(t.x * scale * g.x, t.y * scale * g.y, t.z * scale * g.z,
+                             t.w * scale * g.w));
+  }
 }
 
-// grid: (rows); block: hd/2 threads (one per rotation pair), looping over heads.
+// grid: (rows); block: 256 threads.  Thread t owns rotation frequency i = t % (hd/2) for
+// every head it visits, so one sine/cosine pair per thread serves all its heads.
 template <typename TW, typename TA>
-__global__ void rope_kv_kernel(const float *__restrict__ qkv, TA *__restrict__ q_out,
-                               TreeMeta meta, TW *__restrict__ ck, TW *__restrict__ cv, int n1,
-                               int H, int Hkv, int hd, int capacity,
-                               const double *__restrict__ inv_freq) {
-  const int row = blockIdx.x;
-  const int i = threadIdx.x;  // pair index < hd/2
+__global__ __launch_bounds__(256) void rope_kv_kernel(const float *__restrict__ qkv,
+                                                      TA *__restrict__ q_out, TreeMeta meta,
+                                                      TW *__restrict__ ck, TW *__restrict__ cv,
+                                                      int n1, int H, int Hkv, int hd,
+                                                      int capacity,
+                                                      const double *__restrict__ inv_freq) {
+  const int row = blockIdx.x, tid = threadIdx.x;
   const int half = hd >> 1;
+  const int i = tid % half;
   const int b = row / n1, r = row - b * n1;
   const double ang = (double)meta.pos[row] * inv_freq[i];
   double sd, cd;
@@ -60,23 +100,25 @@ __global__ void rope_kv_kernel(const float *__restrict__ qkv, TA *__restrict__ q
   const float c = (float)cd, s = (float)sd;
   const float *base = qkv + (size_t)row * (H + 2 * Hkv) * hd;
   TA *qo = q_out + (size_t)row * H * hd;
-  for (int h = 0; h < H; ++h) {
-    const float *q = base + h * hd;
-    const float x1 = q[i], x2 = q[i + half];
+  for (int p = tid; p < H * half; p += 256) {
+    const int h = p / half;
+    const float x1 = base[h * hd + i], x2 = base[h * hd + i + half];
     qo[h * hd + i] = from_f32<TA>(x1 * c - x2 * s);
     qo[h * hd + i + half] = from_f32<TA>(x2 * c + x1 * s);
   }
   const int slot = meta.sess_S[b] + r;
-  for (int g = 0; g < Hkv; ++g) {
+  for (int p = tid; p < Hkv * half; p += 256) {
+    const int g = p / half;
     const float *k = base + (H + g) * hd;
-    const float *v = base + (H + Hkv + g) * hd;
     const float x1 = k[i], x2 = k[i + half];
     const size_t kdst = (((size_t)b * Hkv + g) * capacity + slot) * hd;
     ck[kdst + i] = from_f32<TW>(x1 * c - x2 * s);
     ck[kdst + i + half] = from_f32<TW>(x2 * c + x1 * s);
-    const size_t vdst = ((size_t)b * Hkv + g) * hd * capacity + slot;   // [hd][capacity]
-    cv[vdst + (size_t)i * capacity] = from_f32<TW>(v[i]);
-    cv[vdst + (size_t)(i + half) * capacity] = from_f32<TW>(v[i + half]);
+  }
+  for (int e = tid; e < Hkv * hd; e += 256) {   // values: head-dim-major cache
+    const int g = e / hd, dd = e - g * hd;
+    cv[(((size_t)b * Hkv + g) * hd + dd) * capacity + slot] =
+        from_f32<TW>(base[(H + Hkv) * hd + e]);
   }
 }
 
@@ -116,7 +158,7 @@ template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
                           int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s) {
-  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(B * n1), dim3(hd / 2),
+  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(B * n1), dim3(256),
                      0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity,
                      inv_freq);
   return hipGetLastError();
