@@ -6,9 +6,9 @@
 // values of tree row j sit in cache slot prefix_len + j, so one contiguous key range
 // [0, prefix_len + N + 1) covers everything and the mask applies to its tail only.
 //
-// bf16 model.  One workgroup of 8 waves per (key split, kv head, session).  Query rows
-// are the G query heads of the kv head times the N+1 tree rows (row = tree_row * G +
-// head), in 16-row tiles dealt round-robin to the waves (tile = wave + 8 t).  The key
+// bf16 model.  One workgroup of 16 waves (8 with more than 16 tiles) per (key split, kv
+// head, session).  Query rows are the G query heads of the kv head times the N+1 tree rows
+// (row = tree_row * G + head), in 16-row tiles dealt round-robin to the waves.  The key
 // range of the split streams through LDS in chunks of 64 slots:
 //  * HBM -> LDS by direct DMA (global_load_lds, 16 bytes a lane) into a ring of NST
 //    stages.  A stage holds the chunk's keys as [64 slots][head_dim] and its values,
@@ -16,10 +16,11 @@
 //    pieces of every row are XOR-swizzled so that the fragment reads below hit distinct
 //    banks; the DMA fixes where each lane's bytes land, so the swizzle is applied to the
 //    global source addresses.
-//  * One chunk ahead of its use, every thread widens its share of the stage from bf16
-//    to fp16 in place (exact in the fp16 normal range), so the MFMAs run on fp16
-//    operands like the rest of the pass, and zeroes the value columns past the last
-//    tree slot (their probability is 0, but 0 * NaN would not be).
+//  * One chunk ahead of its use, the stage is widened from bf16 to fp16 in place (exact
+//    in the fp16 normal range), so the MFMAs run on fp16 operands like the rest of the
+//    pass, and the value columns past the last tree slot are zeroed (their probability
+//    is 0, but 0 * NaN would not be).  Waves without a query tile do the widening when
+//    there are any, which keeps it off the SIMD that holds two tile waves.
 //  * Scores are computed transposed, S^T = K Q^T with v_mfma_f32_16x16x32_f16 (16 keys
 //    as rows, 16 queries as columns), so each lane holds 16 scores of ONE query.  The
 //    tree mask, the running max (reduced over the query's 4 lanes by two shuffles) and
@@ -41,7 +42,6 @@
 namespace {
 
 constexpr int KC = 64;            // slots per chunk
-constexpr int NWAVES = 8;         // waves per workgroup
 constexpr float LOG2E = 1.4426950408889634f;
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
@@ -64,38 +64,36 @@ template <int HD> AS_DEVICE int k_off(int key, int piece) {
 AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ ((row >> 1) & 7)) << 3); }
 
 // DMA of one chunk (keys key0 .. key0 + 63) into a stage: HD/8 blocks of 1 KB for K and
-// as many for V^T, spread over the 8 waves.
-template <int HD>
+// as many for V^T, dealt to the NW waves in turn.
+template <int HD, int NW>
 AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int key0,
                            int capacity, int wave, int lane) {
   constexpr int BLOCKS = HD / 8;
+  static_assert((2 * BLOCKS) % NW == 0, "DMA blocks per wave");
 #pragma unroll
-  for (int j = 0; j < BLOCKS / NWAVES; ++j) {
-    const int i = wave + NWAVES * j;
-    const int e = i * 512 + lane * 8;          // element offset this lane's bytes land at
-    const int key = e / HD, piece = (e % HD) >> 3;
-    const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
-    dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ sw) << 3), (lds_ptr_t)(stage + i * 512));
-  }
-#pragma unroll
-  for (int j = 0; j < BLOCKS / NWAVES; ++j) {
-    const int i = wave + NWAVES * j;
-    const int row = i * 8 + (lane >> 3), piece = lane & 7;
-    dma16(vb + (size_t)row * capacity + key0 + ((piece ^ ((row >> 1) & 7)) << 3),
-          (lds_ptr_t)(stage + KC * HD + i * 512));
+  for (int j = 0; j < 2 * BLOCKS / NW; ++j) {
+    const int blk = wave + NW * j;
+    if (blk < BLOCKS) {
+      const int e = blk * 512 + lane * 8;          // element offset this lane's bytes land at
+      const int key = e / HD, piece = (e % HD) >> 3;
+      const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
+      dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ sw) << 3), (lds_ptr_t)(stage + blk * 512));
+    } else {
+      const int i = blk - BLOCKS;
+      const int row = i * 8 + (lane >> 3), piece = lane & 7;
+      dma16(vb + (size_t)row * capacity + key0 + ((piece ^ ((row >> 1) & 7)) << 3),
+            (lds_ptr_t)(stage + KC * HD + i * 512));
+    }
   }
 }
 
-// bf16 -> fp16 in place for this thread's pieces of a stage; value slots >= total are
-// zeroed.
+// bf16 -> fp16 in place for pieces t, t + stride, ... of a stage (t: the thread's index
+// among the widening threads); value slots >= total are zeroed.
 template <int HD>
-AS_DEVICE void widen_chunk(uint16_t *stage, int tid, int key0, int total) {
+AS_DEVICE void widen_chunk(uint16_t *stage, int t, int stride, int key0, int total) {
   constexpr int KPIECES = KC * HD / 8;
-  constexpr int PER = 2 * KPIECES / (NWAVES * 64);
   const bool tail = key0 + KC > total;
-#pragma unroll
-  for (int j = 0; j < PER; ++j) {
-    const int pc = tid + j * NWAVES * 64;
+  for (int pc = t; pc < 2 * KPIECES; pc += stride) {
     uint16_t *p = stage + pc * 8;
     f16x8 h = bf16x8_to_f16x8(*(const bf16x8 *)p);
     if (tail && pc >= KPIECES) {
@@ -109,14 +107,14 @@ AS_DEVICE void widen_chunk(uint16_t *stage, int tid, int key0, int total) {
   }
 }
 
-template <int HD, int TPW, int NST>
-__global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
+template <int HD, int NW, int UPW, int NST>
+__global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     const f16 *__restrict__ qin, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
     TreeMeta meta, f16 *__restrict__ out, float *__restrict__ part_o,
     float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit) {
   constexpr int KSTEPS = HD / 32, NB = HD / 16;
   constexpr int STAGE = 2 * KC * HD;     // elements: K [KC][HD], then V^T [HD][KC]
-  constexpr int L_DMA = HD / 32;         // DMA instructions per wave per chunk
+  constexpr int L_DMA = HD / 4 / NW;     // DMA instructions per wave per chunk
   static_assert(NST >= 3, "the widening runs one stage ahead of the MFMAs");
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
 
@@ -137,14 +135,15 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
   const int q_stride = H * HD;
   const float sscale = LOG2E / sqrtf((float)HD);   // scores -> base-2 exponent
 
-  // Query fragments (B operand of S^T = K Q^T), tree-ancestor masks, softmax state.
-  f16x8 qf[TPW][KSTEPS];
-  uint64_t anc[TPW];
-  float m_run[TPW], l_run[TPW];
-  f32x4 o[TPW][NB];
+  // Query tile t of this wave: wave + NW t.  Per tile: query fragments (B operand of
+  // S^T = K Q^T), ancestor mask, running softmax state.
+  f16x8 qf[UPW][KSTEPS];
+  uint64_t anc[UPW];
+  float m_run[UPW], l_run[UPW];
+  f32x4 o[UPW][NB];
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    int qi = (wave + NWAVES * t) * 16 + lr;
+  for (int t = 0; t < UPW; ++t) {
+    int qi = (wave + NW * t) * 16 + lr;
     qi = qi < QR ? qi : QR - 1;
     const int r = qi / G, h = g * G + (qi - r * G);
     const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
@@ -159,15 +158,20 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
   wait_vmcnt<0>();   // the loop's vmcnt accounting covers the DMA only
 
   auto stage_of = [&](int c) { return smem + ((c - c0) % NST) * STAGE; };
+  // The widening goes to the waves without a tile when there are any (one SIMD then
+  // holds no more than its share of tile work plus widening), else to every wave.
+  const int wbeg = ntiles < NW ? ntiles : 0;
+  const int wt = (wave - wbeg) * 64 + lane, wstride = (NW - wbeg) * 64;
+  const bool widener = wave >= wbeg;
 
   // Prologue: chunks c0 .. c0+NST-2 in flight, chunk c0 widened.
 #pragma unroll
   for (int i = 0; i < NST - 1; ++i)
-    if (c0 + i < c1) issue_chunk<HD>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
+    if (c0 + i < c1) issue_chunk<HD, NW>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
   if (c0 < c1) {
     if (c0 + NST - 2 < c1) wait_vmcnt<(NST - 2) * L_DMA>(); else wait_vmcnt<0>();
     lds_barrier();
-    widen_chunk<HD>(stage_of(c0), tid, c0 * KC, total);
+    if (widener) widen_chunk<HD>(stage_of(c0), wt, wstride, c0 * KC, total);
   }
 
   for (int c = c0; c < c1; ++c) {
@@ -176,8 +180,8 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
     }
     lds_barrier();
     if (c + NST - 1 < c1)
-      issue_chunk<HD>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity, wave, lane);
-    if (c + 1 < c1) widen_chunk<HD>(stage_of(c + 1), tid, (c + 1) * KC, total);
+      issue_chunk<HD, NW>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity, wave, lane);
+    if (c + 1 < c1 && widener) widen_chunk<HD>(stage_of(c + 1), wt, wstride, (c + 1) * KC, total);
 
     const uint16_t *st = stage_of(c);
     const f16 *sk = (const f16 *)st;
@@ -185,37 +189,37 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
     const int key0 = c * KC;
     const bool tree_chunk = key0 + KC > S;
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-      if (wave + NWAVES * t >= ntiles) break;
-      // S^T for 4 blocks of 16 keys: sc[kb][e] is the score of slot key0 + kb*16 + lg*4
+    for (int t = 0; t < UPW; ++t) {
+      if (wave + NW * t >= ntiles) break;
+      // S^T for 4 blocks of 16 keys: sc[kk][e] is the score of slot key0 + kk*16 + lg*4
       // + e against this lane's query.
       f32x4 sc[4];
 #pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4) sc[k4] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kk = 0; kk < 4; ++kk) sc[kk] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s)
 #pragma unroll
-        for (int k4 = 0; k4 < 4; ++k4) {
-          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(k4 * 16 + lr, s * 4 + lg));
-          sc[k4] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[k4], 0, 0, 0);
+        for (int kk = 0; kk < 4; ++kk) {
+          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(kk * 16 + lr, s * 4 + lg));
+          sc[kk] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[kk], 0, 0, 0);
         }
       if (tree_chunk) {
 #pragma unroll
-        for (int k4 = 0; k4 < 4; ++k4)
+        for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            // slot key0 + k4*16 + lg*4 + e is tree row j (prefix slot if j < 0)
-            const int j = key0 + k4 * 16 + lg * 4 + e - S;
+            // the slot is tree row j (a prefix slot if j < 0)
+            const int j = key0 + kk * 16 + lg * 4 + e - S;
             const int sh = min(max(j - 1, 0), 63);
             const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((anc[t] >> sh) & 1ull)));
-            sc[k4][e] = vis ? sc[k4][e] : -INFINITY;
+            sc[kk][e] = vis ? sc[kk][e] : -INFINITY;
           }
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4)
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[k4][e]);
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[kk][e]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float m_new = fmaxf(m_run[t], mx);
@@ -227,12 +231,12 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
       f16x8 pb[2];
       float rs = 0.f;
 #pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4)
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[k4][e], sscale, -mb));
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[kk][e], sscale, -mb));
           rs += p;
-          pb[k4 >> 1][(k4 & 1) * 4 + e] = (f16)p;
+          pb[kk >> 1][(kk & 1) * 4 + e] = (f16)p;
         }
       l_run[t] = l_run[t] * alpha + rs;
       if (__ballot(alpha < 1.f)) {
@@ -243,14 +247,14 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
       }
       // O^T += V^T P^T over two k-steps of 32 keys.
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
+      for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           const int row = nb * 16 + lr;
-          const f16x4 lo = *(const f16x4 *)(sv + v_off(row, s2 * 4 + (lg >> 1)) + (lg & 1) * 4);
-          const f16x4 hi = *(const f16x4 *)(sv + v_off(row, s2 * 4 + 2 + (lg >> 1)) + (lg & 1) * 4);
+          const f16x4 lo = *(const f16x4 *)(sv + v_off(row, ks * 4 + (lg >> 1)) + (lg & 1) * 4);
+          const f16x4 hi = *(const f16x4 *)(sv + v_off(row, ks * 4 + 2 + (lg >> 1)) + (lg & 1) * 4);
           const f16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[s2], o[t][nb], 0, 0, 0);
+          o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[ks], o[t][nb], 0, 0, 0);
         }
     }
   }
@@ -258,8 +262,8 @@ __global__ __launch_bounds__(NWAVES * 64) void tree_attn_mfma_kernel(
 
   // o[t][nb][e] is head dim nb*16 + lg*4 + e of query tile*16 + lr.
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const int tile = wave + NWAVES * t;
+  for (int t = 0; t < UPW; ++t) {
+    const int tile = wave + NW * t;
     if (tile >= ntiles) break;
     float l = l_run[t];
     l += __shfl_xor(l, 16);
@@ -348,16 +352,15 @@ __global__ __launch_bounds__(64) void tree_attn_f32_kernel(
   if (lane + 64 < HD) op[lane + 64] = o1 / l;
 }
 
-// Ring depth per head dim: 4 stages of 32 KB (head_dim 128, one workgroup per CU) or of
-// 16 KB (head_dim 64, two per CU).
+// Ring depth: 4 stages of 32 KB (head_dim 128) or 16 KB (head_dim 64).
 template <int HD> struct AttnCfg { static constexpr int NST = 4; };
 
-template <int HD, int TPW>
+template <int HD, int NW, int UPW>
 void launch_mfma(dim3 grid, hipStream_t s, const f16 *q, const bf16 *ck, const bf16 *cv,
                  const TreeMeta &meta, f16 *out, float *po, float *pml, int n1, int H, int Hkv,
                  int capacity, int nsplit) {
-  hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, TPW, AttnCfg<HD>::NST>), grid,
-                     dim3(NWAVES * 64), 0, s, q, ck, cv, meta, out, po, pml, n1, H, Hkv,
+  hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, NW, UPW, AttnCfg<HD>::NST>), grid,
+                     dim3(NW * 64), 0, s, q, ck, cv, meta, out, po, pml, n1, H, Hkv,
                      capacity, nsplit);
 }
 
@@ -373,11 +376,14 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
                                   int *nsplit_used) {
   const int G = H / Hkv, QR = G * n1;
   const int tiles = (QR + 15) / 16;
-  const int tpw = (tiles + NWAVES - 1) / NWAVES;
-  if (tpw > 4 || capacity % KC != 0) return hipErrorInvalidValue;
-  // Key splits so that every resident workgroup slot of the chip gets work (one
-  // workgroup per CU at head_dim 128, two at 64), keeping at least 4 chunks per split.
-  const int slots = cus * (hd == 128 ? 1 : 2);
+  // Up to 16 tiles: 16 waves, one tile per wave, the others widen (measured fastest on
+  // the 8B shape: 5 tiles); more tiles: 8 waves with up to 4 tiles each.
+  const int nw = tiles <= 16 ? 16 : 8;
+  const int upw = (tiles + nw - 1) / nw;
+  if (upw > 4 || capacity % KC != 0) return hipErrorInvalidValue;
+  // Key splits so that every resident workgroup slot of the chip gets work (one 16-wave
+  // workgroup per CU; two 8-wave ones at head_dim 64), keeping at least 4 chunks per split.
+  const int slots = cus * (nw == 8 && hd == 64 ? 2 : 1);
   const int items = B * Hkv;
   const int nchunks = capacity / KC;
   int nsplit = (slots + items - 1) / items;
@@ -386,13 +392,15 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
   while (nsplit > 1 && (long long)items * nsplit * QR * hd > part_capacity) --nsplit;
   *nsplit_used = nsplit;
   const dim3 grid(nsplit, Hkv, B);
-#define GO(HD_, TPW_)                                                                     \
-  launch_mfma<HD_, TPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,      \
-                         capacity, nsplit)
+#define GO(HD_, NW_, UPW_)                                                                \
+  launch_mfma<HD_, NW_, UPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,  \
+                              capacity, nsplit)
   if (hd == 128) {
-    if (tpw == 1) GO(128, 1); else if (tpw == 2) GO(128, 2); else if (tpw == 3) GO(128, 3); else GO(128, 4);
+    if (nw == 16) GO(128, 16, 1);
+    else if (upw == 2) GO(128, 8, 2); else if (upw == 3) GO(128, 8, 3); else GO(128, 8, 4);
   } else {
-    if (tpw == 1) GO(64, 1); else if (tpw == 2) GO(64, 2); else if (tpw == 3) GO(64, 3); else GO(64, 4);
+    if (nw == 16) GO(64, 16, 1);
+    else if (upw == 2) GO(64, 8, 2); else if (upw == 3) GO(64, 8, 3); else GO(64, 8, 4);
   }
 #undef GO
   hipError_t e = hipGetLastError();
