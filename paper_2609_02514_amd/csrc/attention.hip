@@ -23,10 +23,10 @@
 //    there are any, which keeps it off the SIMD that holds two tile waves.
 //  * Scores are computed transposed, S^T = K Q^T with v_mfma_f32_16x16x32_f16 (16 keys
 //    as rows, 16 queries as columns), so each lane holds 16 scores of ONE query.  The
-//    tree mask, the running max (reduced over the query's 4 lanes by two shuffles) and
+//    tree mask, the running max (reduced over the query's 4 lanes by two row swaps) and
 //    exp2 stay in the lane, and the lane's probabilities, rounded to fp16, are exactly
-//    its B operand of O^T = V^T P^T: the contraction order over the chunk's keys is a
-//    permutation shared with the V fragments (two 8-byte LDS reads a lane).  The O^T
+//    its B operand of O^T = V^T P^T (the keys are assigned to MFMA rows so that a lane's
+//    8 probabilities are 8 consecutive keys, whose V^T fragment is one 16-byte read).  The O^T
 //    accumulator lane holds 4 head dims of its query, so the online-softmax rescale is
 //    lane-local (and skipped when no running max moved).
 //  * Barrier protocol at chunk c: a wave waits for its own DMA of chunk c+1; one LDS
@@ -52,16 +52,31 @@ AS_DEVICE bool tree_visible(int slot, int S, int n1, uint64_t anc) {
   return j == 0 || ((anc >> (j - 1)) & 1ull);
 }
 
-// Element offset of 16-byte piece `piece` of key row `key` in a stage's K part.  A key
-// row is HD * 2 bytes; the swizzle spreads 16 consecutive keys over the 16 distinct
-// 16-byte bank groups of a 256-byte window.
+// Order of the keys inside each 32-key group of a chunk: A row m of key block kk (16
+// rows) holds key (kk/2)*32 + (m/4)*8 + (kk%2)*4 + m%4.  The score block's output row
+// lg*4 + e is then key (kk/2)*32 + lg*8 + (kk%2)*4 + e, so the lane with row group lg
+// holds the 8 consecutive keys (kk/2)*32 + lg*8 .. + 7 of its query -- one contiguous
+// 16-byte read of a V^T row gives its A operand of O^T = V^T P^T.
+AS_DEVICE int key_of_row(int kk, int m) { return (kk >> 1) * 32 + (m >> 2) * 8 + (kk & 1) * 4 + (m & 3); }
+AS_DEVICE int key_of_score(int kk, int lg, int e) { return (kk >> 1) * 32 + lg * 8 + (kk & 1) * 4 + e; }
+
+// XOR swizzles of the 16-byte pieces of a row, chosen so that each fragment read -- 16
+// lanes at one logical piece of 16 rows (keys m = 0..15 of a block above, or 16
+// consecutive V^T rows) -- touches distinct banks whether the LDS serves 16 lanes (64
+// banks) or 8 lanes (32 banks) of a 16-byte read per cycle.  K rows are 2*HD bytes.
+template <int HD> AS_DEVICE int ksw(int key) {
+  if (HD == 128) return (((key >> 3) & 3) << 2) | (key & 3);
+  return ((key & 1) ^ ((key >> 4) & 1)) | (((key >> 1) & 1) << 1) | (((key >> 3) & 1) << 2);
+}
+AS_DEVICE int vsw(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+// Element offset of piece `piece` of key row `key` in a stage's K part.
 template <int HD> AS_DEVICE int k_off(int key, int piece) {
-  const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
-  return key * HD + ((piece ^ sw) << 3);
+  return key * HD + ((piece ^ ksw<HD>(key)) << 3);
 }
 // Element offset of piece `piece` (8 slots) of head-dim row `row` in a stage's V^T part
-// (rows of 64 slots = 128 bytes, two rows per 256-byte window).
-AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ ((row >> 1) & 7)) << 3); }
+// (rows of 64 slots = 128 bytes).
+AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ vsw(row)) << 3); }
 
 // DMA of one chunk (keys key0 .. key0 + 63) into a stage: HD/8 blocks of 1 KB for K and
 // as many for V^T, dealt to the NW waves in turn.
@@ -76,12 +91,12 @@ AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int 
     if (blk < BLOCKS) {
       const int e = blk * 512 + lane * 8;          // element offset this lane's bytes land at
       const int key = e / HD, piece = (e % HD) >> 3;
-      const int sw = HD == 128 ? (key & 15) : ((key >> 1) & 7);
-      dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ sw) << 3), (lds_ptr_t)(stage + blk * 512));
+      dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ ksw<HD>(key)) << 3),
+            (lds_ptr_t)(stage + blk * 512));
     } else {
       const int i = blk - BLOCKS;
       const int row = i * 8 + (lane >> 3), piece = lane & 7;
-      dma16(vb + (size_t)row * capacity + key0 + ((piece ^ ((row >> 1) & 7)) << 3),
+      dma16(vb + (size_t)row * capacity + key0 + ((piece ^ vsw(row)) << 3),
             (lds_ptr_t)(stage + KC * HD + i * 512));
     }
   }
@@ -98,7 +113,7 @@ AS_DEVICE void widen_chunk(uint16_t *stage, int t, int stride, int key0, int tot
     f16x8 h = bf16x8_to_f16x8(*(const bf16x8 *)p);
     if (tail && pc >= KPIECES) {
       const int vp = pc - KPIECES, row = vp >> 3;
-      const int s0 = key0 + (((vp & 7) ^ ((row >> 1) & 7)) << 3);
+      const int s0 = key0 + (((vp & 7) ^ vsw(row)) << 3);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (s0 + e >= total) h[e] = (f16)0.f;
@@ -191,8 +206,8 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
 #pragma unroll
     for (int t = 0; t < UPW; ++t) {
       if (wave + NW * t >= ntiles) break;
-      // S^T for 4 blocks of 16 keys: sc[kk][e] is the score of slot key0 + kk*16 + lg*4
-      // + e against this lane's query.
+      // S^T for 4 blocks of 16 keys: sc[kk][e] is the score of slot
+      // key0 + key_of_score(kk, lg, e) against this lane's query.
       f32x4 sc[4];
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) sc[kk] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -200,7 +215,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       for (int s = 0; s < KSTEPS; ++s)
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(kk * 16 + lr, s * 4 + lg));
+          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(key_of_row(kk, lr), s * 4 + lg));
           sc[kk] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[kk], 0, 0, 0);
         }
       if (tree_chunk) {
@@ -209,7 +224,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             // the slot is tree row j (a prefix slot if j < 0)
-            const int j = key0 + kk * 16 + lg * 4 + e - S;
+            const int j = key0 + key_of_score(kk, lg, e) - S;
             const int sh = min(max(j - 1, 0), 63);
             const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((anc[t] >> sh) & 1ull)));
             sc[kk][e] = vis ? sc[kk][e] : -INFINITY;
@@ -220,8 +235,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
         for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[kk][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = rows4_max(mx);
       const float m_new = fmaxf(m_run[t], mx);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       // raw v_exp_f32: results below 2^-126 flush to zero, which a softmax weight can spare
@@ -250,10 +264,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const int row = nb * 16 + lr;
-          const f16x4 lo = *(const f16x4 *)(sv + v_off(row, ks * 4 + (lg >> 1)) + (lg & 1) * 4);
-          const f16x4 hi = *(const f16x4 *)(sv + v_off(row, ks * 4 + 2 + (lg >> 1)) + (lg & 1) * 4);
-          const f16x8 va = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          const f16x8 va = *(const f16x8 *)(sv + v_off(nb * 16 + lr, ks * 4 + lg));
           o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[ks], o[t][nb], 0, 0, 0);
         }
     }
@@ -265,9 +276,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   for (int t = 0; t < UPW; ++t) {
     const int tile = wave + NW * t;
     if (tile >= ntiles) break;
-    float l = l_run[t];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    const float l = rows4_sum(l_run[t]);
     const int qi = tile * 16 + lr;
     if (qi >= QR) continue;
     const int r = qi / G, h = g * G + (qi - r * G);
