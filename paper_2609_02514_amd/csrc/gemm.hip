@@ -338,9 +338,10 @@ using acespec::EPI_F32;
 // Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU,
 // k per stage}.  Measured on MI355X against the verify-step shapes.  Tried and slower on
 // every shape here: ping-pong pairs of waves per SIMD (one issuing 32 x 32 MFMAs while
-// the other loads), deeper rings (5-8 stages) at one workgroup per CU, 128 x 128 tiles
-// with 64-wide k stages, and fp16 weights (which only removes the in-register widening,
-// worth 3-8 %).  The limit of the 128 x 256 tiling is the L2 -> LDS path, not the MFMA
+// the other loads), deeper rings (5-8 stages) at one workgroup per CU, with 64 x 64 wave
+// tiles or 128 x 512 block tiles, 128 x 128 tiles with 64-wide k stages, fp16 weights
+// (which only removes the in-register widening, worth 3-8 %), and weights and
+// activations pre-packed into 1 KB tile blocks (contiguous DMA; 2-9 %).  The limit of the 128 x 256 tiling is the L2 -> LDS path, not the MFMA
 // pipe: with the DMA removed it runs at 1.9 PFLOP/s, with the MFMAs removed at 75 % of
 // its full time.
 struct GemmVariant {
@@ -350,6 +351,7 @@ constexpr GemmVariant kVariants[] = {
     {1, 4, 8, 4, 3, 2, 32},   // 0: 128 x 256, 4 waves of 128 x 64, 72 KB LDS, 2 WGs per CU
     {2, 2, 4, 4, 4, 2, 32},   // 1: 128 x 128, 4 waves of 64 x 64, 64 KB LDS, 2 WGs per CU
     {2, 4, 4, 4, 3, 1, 64},   // 2: 128 x 256, 8 waves of 64 x 64, k 64, 144 KB LDS, 1 WG per CU
+    {2, 4, 8, 4, 4, 1, 32},   // 3: 256 x 256, 8 waves of 128 x 64, 128 KB LDS, 1 WG per CU
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -384,7 +386,7 @@ void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const TB *W, in
                 int K, f16 *out, float *outf, float *part, int mt, int nt, int splits) {
   switch (var) {
 #define CASE(V) case V: launch_variant<EPI, V, TB>(grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    CASE(0) CASE(1) CASE(2)
+    CASE(0) CASE(1) CASE(2) CASE(3)
 #undef CASE
     default: break;
   }
@@ -392,11 +394,15 @@ void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const TB *W, in
 
 // Default tiling per shape (measured on MI355X): 128 x 128 tiles for few rows (more
 // tiles to spread over 256 CUs), the 8-wave 64-wide-k tiling for QKV-sized fp32
-// outputs, 128 x 256 otherwise.
+// outputs, 256 x 256 tiles (a third fewer operand bytes per flop, two stages in flight)
+// for the residual and LM-head products once there are enough rows, 128 x 256
+// otherwise -- for the gate/up product 256 x 256 tiles leave the last of three rounds
+// of workgroups mostly empty.
 int pick_variant(int epi, int M, int N, int K) {
   (void)K;
   if (M <= 384) return 1;
   if (epi == EPI_F32 && N <= 8192) return 2;
+  if (M >= 1024 && (epi == EPI_RESID || epi == EPI_F32)) return 3;
   return 0;
 }
 
