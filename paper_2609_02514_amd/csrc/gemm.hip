@@ -66,7 +66,7 @@ template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
-    int splits) {
+    int full, int tsplit) {
   constexpr int NW = WMN * WNN;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
   constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
@@ -82,14 +82,25 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE_BYTES];
   typedef typename Vec8<TB>::type tbx8;
 
-  const int units = mt * nt * splits;
-  const int unit = xcd_tile(blockIdx.x, units);
-  const int tn = unit / (mt * splits);
-  const int rem = unit - tn * (mt * splits);
-  const int tm = rem / splits, sp = rem - tm * splits;
+  // Units: `full` whole tiles, then tsplit k-slices of each remaining tile (their partial
+  // sums go to `part`, summed by tile_fixup_kernel).  Each group is dealt over the XCDs on
+  // its own (full is a multiple of 8), so the slices spread over the whole chip.
+  const int tiles = mt * nt;
+  int tile, sp, ns;
+  if ((int)blockIdx.x < full) {
+    tile = xcd_tile(blockIdx.x, full);
+    sp = 0;
+    ns = 1;
+  } else {
+    const int u = xcd_tile(blockIdx.x - full, (tiles - full) * tsplit);
+    tile = full + u / tsplit;
+    sp = u - (tile - full) * tsplit;
+    ns = tsplit;
+  }
+  const int tn = tile / mt, tm = tile - tn * mt;
   const int m0 = tm * TBM;
   const int KT = K / KSS;
-  const int kt0 = (int)((long long)KT * sp / splits), kt1 = (int)((long long)KT * (sp + 1) / splits);
+  const int kt0 = (int)((long long)KT * sp / ns), kt1 = (int)((long long)KT * (sp + 1) / ns);
   const int nk = kt1 - kt0;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -209,7 +220,24 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   wait_vmcnt<0>();
 
   // Epilogue.  acc[i][j][e] is C[row = m0 + wm*WTM*16 + i*16 + lk*4 + e][col = .. + lr].
-  const size_t MN = (size_t)M * N;
+  if (ns > 1) {  // k-slice of a split tile: raw sums at [slice][tile row][W-tile row]
+    float *pt = part + ((size_t)(tile - full) * ns + sp) * (TBM * TBN);
+#pragma unroll
+    for (int ii = 0; ii < WTM; ++ii)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int lrow = wm * WTM * 16 + ii * 16 + lk * 4 + e;
+#pragma unroll
+        for (int j = 0; j < WTN; ++j) {
+          const int tc = (EPI == acespec::EPI_SWIGLU)
+                             ? (j < HALF ? wn * HALF * 16 + j * 16
+                                         : TBN / 2 + wn * HALF * 16 + (j - HALF) * 16) + lr
+                             : wn * WTN * 16 + j * 16 + lr;
+          pt[lrow * TBN + tc] = acc[ii][j][e];
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int ii = 0; ii < WTM; ++ii) {
 #pragma unroll
@@ -229,8 +257,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
           const int col = tn * TBN + wn * WTN * 16 + j * 16 + lr;
           if (col >= N) continue;
           const size_t o = (size_t)row * N + col;
-          if (splits > 1) part[sp * MN + o] = acc[ii][j][e];
-          else if (EPI == acespec::EPI_STORE) out[o] = (f16)acc[ii][j][e];
+          if (EPI == acespec::EPI_STORE) out[o] = (f16)acc[ii][j][e];
           else if (EPI == acespec::EPI_RESID) outf[o] += acc[ii][j][e];
           else outf[o] = acc[ii][j][e];
         }
@@ -239,21 +266,46 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   }
 }
 
-// Split-K reduction in a fixed order (deterministic): dst (+)= sum_s part[s].
-template <bool RESID>
-__global__ void splitk_reduce_kernel(const float4 *__restrict__ part, float4 *__restrict__ dst,
-                                     size_t n4, int splits) {
-  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n4) return;
-  float4 acc = RESID ? dst[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < splits; ++s) {
-    const float4 v = part[s * n4 + i];
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
+// Sums the k-slices of the split tiles in a fixed order (deterministic) and applies the
+// epilogue.  One thread per 4 adjacent tile columns of one tile row (SwiGLU: 4 gate
+// columns and the matching 4 up columns).
+template <int EPI, int TBM, int TBN>
+__global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict__ part,
+                                                         f16 *__restrict__ out,
+                                                         float *__restrict__ outf, int M, int N,
+                                                         int mt, int full, int nsplit_tiles,
+                                                         int tsplit) {
+  constexpr int CW = (EPI == acespec::EPI_SWIGLU ? TBN / 2 : TBN) / 4;  // threads per row
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (long long)nsplit_tiles * TBM * CW) return;
+  const int t = (int)(gid / (TBM * CW));
+  const int rem = (int)(gid - (long long)t * TBM * CW);
+  const int lrow = rem / CW, c4 = (rem - lrow * CW) * 4;
+  const int tile = full + t, tn = tile / mt, tm = tile - tn * mt;
+  const int row = tm * TBM + lrow;
+  if (row >= M) return;
+  const float *pt = part + (size_t)t * tsplit * (TBM * TBN) + (size_t)lrow * TBN + c4;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), g = a;
+  for (int sp = 0; sp < tsplit; ++sp) {
+    const float4 v = *(const float4 *)(pt + (size_t)sp * (TBM * TBN));
+    a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
+    if (EPI == acespec::EPI_SWIGLU) {
+      const float4 u = *(const float4 *)(pt + (size_t)sp * (TBM * TBN) + TBN / 2);
+      g.x += u.x; g.y += u.y; g.z += u.z; g.w += u.w;
+    }
   }
-  dst[i] = acc;
+  const float av[4] = {a.x, a.y, a.z, a.w}, uv[4] = {g.x, g.y, g.z, g.w};
+  const int col0 = tn * (EPI == acespec::EPI_SWIGLU ? TBN / 2 : TBN) + c4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int col = col0 + q;
+    if (col >= N) continue;
+    const size_t o = (size_t)row * N + col;
+    if (EPI == acespec::EPI_SWIGLU) out[o] = (f16)silu_mul(av[q], uv[q]);
+    else if (EPI == acespec::EPI_STORE) out[o] = (f16)av[q];
+    else if (EPI == acespec::EPI_RESID) outf[o] += av[q];
+    else outf[o] = av[q];
+  }
 }
 
 // ------------------------------------------------------------------------------------
@@ -355,37 +407,69 @@ constexpr GemmVariant kVariants[] = {
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
-// Chooses the number of K splits: enough units to fill the chip, weighed against the
-// cost of re-reading fp32 partials.  Only residual / fp32 epilogues split.
-int choose_splits(int epi, int M, int N, int K, int tiles, int cus, int occ) {
-  if (epi == EPI_SWIGLU || epi == EPI_STORE || (N % 4) != 0) return 1;
-  const int KT = K / 64;
-  const double part_cost = (double)M * N * 4 / 10e12 / 0.43e-6;  // per split, in 64-k units
+// Work split of a product: `full` whole tiles, then `tsplit` k-slices of each of the
+// remaining tiles.  With at least one round of whole tiles, only the tiles of the last,
+// partly empty round are sliced (enough slices to fill it); with fewer tiles than
+// workgroup slots every tile is sliced, weighing the fill against the cost of the fp32
+// partials.
+struct SplitPlan {
+  int full, tsplit;
+};
+SplitPlan plan_split(int M, int N, int K, int kss, int tbm, int tbn, int tiles, int cus, int occ,
+                     long long part_cap) {
+  const int slots = cus * occ;
+  const int KT = K / kss;
+  SplitPlan p{tiles, 1};
+  if (tiles >= slots) {
+    const int full = tiles / slots * slots, rest = tiles - full;
+    if (rest == 0) return p;
+    int sl = slots / rest;
+    if (sl > 8) sl = 8;
+    while (sl > 1 && KT / sl < 8) --sl;
+    while (sl > 1 && (long long)rest * sl * tbm * tbn > part_cap) --sl;
+    if (sl > 1) p = SplitPlan{full, sl};
+    return p;
+  }
+  const double part_cost = (double)M * N * 4 / 10e12 / 0.43e-6 * (64.0 / kss);  // per slice
   int best = 1;
   double best_t = 1e30;
-  for (int s = 1; s <= 8; ++s) {
-    if (KT / s < 4) break;
-    const double rounds = std::ceil((double)tiles * s / ((double)cus * occ));
-    const double t = rounds * std::ceil((double)KT / s) + (s > 1 ? part_cost * s : 0.0);
-    if (t < best_t * 0.97) { best_t = t; best = s; }
+  for (int sl = 1; sl <= 8; ++sl) {
+    if (KT / sl < 4) break;
+    if ((long long)tiles * sl * tbm * tbn > part_cap) break;
+    const double rounds = std::ceil((double)tiles * sl / slots);
+    const double t = rounds * std::ceil((double)KT / sl) + (sl > 1 ? part_cost * sl : 0.0);
+    if (t < best_t * 0.97) { best_t = t; best = sl; }
   }
-  return best;
+  if (best > 1) p = SplitPlan{0, best};
+  return p;
 }
 
 template <int EPI, int V, typename TB>
-void launch_variant(dim3 grid, hipStream_t s, const f16 *A, const TB *W, int M, int N, int K,
-                    f16 *out, float *outf, float *part, int mt, int nt, int splits) {
+void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int K, f16 *out,
+                    float *outf, float *part, int mt, int nt, SplitPlan sp) {
   constexpr GemmVariant v = kVariants[V];
+  constexpr int TBM = v.wmn * v.wtm * 16, TBN = v.wnn * v.wtn * 16;
+  const int tiles = mt * nt;
+  const int units = sp.full + (tiles - sp.full) * sp.tsplit;
   hipLaunchKernelGGL(
-        (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>), grid,
-        dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
+        (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>),
+        dim3(units), dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
+        sp.full, sp.tsplit);
+  if (sp.tsplit > 1) {
+    const int nsplit_tiles = tiles - sp.full;
+    const long long threads =
+        (long long)nsplit_tiles * TBM * ((EPI == EPI_SWIGLU ? TBN / 2 : TBN) / 4);
+    hipLaunchKernelGGL((tile_fixup_kernel<EPI, TBM, TBN>), dim3((threads + 255) / 256),
+                       dim3(256), 0, s, part, out, outf, M, N, mt, sp.full, nsplit_tiles,
+                       sp.tsplit);
+  }
 }
 
 template <int EPI, typename TB>
-void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const TB *W, int M, int N,
-                int K, f16 *out, float *outf, float *part, int mt, int nt, int splits) {
+void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N, int K,
+                f16 *out, float *outf, float *part, int mt, int nt, SplitPlan sp) {
   switch (var) {
-#define CASE(V) case V: launch_variant<EPI, V, TB>(grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
+#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp); break;
     CASE(0) CASE(1) CASE(2) CASE(3)
 #undef CASE
     default: break;
@@ -395,14 +479,14 @@ void launch_epi(int var, dim3 grid, hipStream_t s, const f16 *A, const TB *W, in
 // Default tiling per shape (measured on MI355X): 128 x 128 tiles for few rows (more
 // tiles to spread over 256 CUs), the 8-wave 64-wide-k tiling for QKV-sized fp32
 // outputs, 256 x 256 tiles (a third fewer operand bytes per flop, two stages in flight)
-// for the residual and LM-head products once there are enough rows, 128 x 256
-// otherwise -- for the gate/up product 256 x 256 tiles leave the last of three rounds
-// of workgroups mostly empty.
+// for the residual and LM-head products once there are enough rows, 128 x 256 otherwise
+// (for the gate/up product at ~1k rows both tilings measure the same, the 256 x 256 one
+// only with its last round sliced).
 int pick_variant(int epi, int M, int N, int K) {
   (void)K;
   if (M <= 384) return 1;
   if (epi == EPI_F32 && N <= 8192) return 2;
-  if (M >= 1024 && (epi == EPI_RESID || epi == EPI_F32)) return 3;
+  if (M >= 1024 && epi != EPI_SWIGLU) return 3;
   return 0;
 }
 
@@ -420,26 +504,18 @@ hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm;
   const int nt = epi == EPI_SWIGLU ? (N + tbn / 2 - 1) / (tbn / 2) : (N + tbn - 1) / tbn;
-  int splits = splits_override > 0 ? splits_override
-                                   : choose_splits(epi, M, N, K, mt * nt, cus, v.occ);
-  if (epi == EPI_SWIGLU || epi == EPI_STORE || (N % 4) != 0) splits = 1;
-  while (splits > 1 && (long long)splits * M * N > part_cap) --splits;
-  const dim3 grid(mt * nt * splits);
+  const int tiles = mt * nt;
+  SplitPlan sp = plan_split(M, N, K, v.kss, tbm, tbn, tiles, cus, v.occ, part_cap);
+  if (splits_override == 1) sp = SplitPlan{tiles, 1};
+  else if (splits_override > 1 &&
+           (long long)tiles * splits_override * tbm * tbn <= part_cap)
+    sp = SplitPlan{0, splits_override};
   switch (epi) {
-    case EPI_STORE: launch_epi<EPI_STORE, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    case EPI_RESID: launch_epi<EPI_RESID, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    case EPI_SWIGLU: launch_epi<EPI_SWIGLU, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits); break;
-    default: launch_epi<EPI_F32, TB>(var, grid, s, A, W, M, N, K, out, outf, part, mt, nt, splits);
+    case EPI_STORE: launch_epi<EPI_STORE, TB>(var, s, A, W, M, N, K, out, outf, part, mt, nt, sp); break;
+    case EPI_RESID: launch_epi<EPI_RESID, TB>(var, s, A, W, M, N, K, out, outf, part, mt, nt, sp); break;
+    case EPI_SWIGLU: launch_epi<EPI_SWIGLU, TB>(var, s, A, W, M, N, K, out, outf, part, mt, nt, sp); break;
+    default: launch_epi<EPI_F32, TB>(var, s, A, W, M, N, K, out, outf, part, mt, nt, sp);
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
-  const size_t n4 = (size_t)M * N / 4;
-  if (epi == EPI_RESID)
-    hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3((n4 + 255) / 256), dim3(256), 0, s,
-                       (const float4 *)part, (float4 *)outf, n4, splits);
-  else
-    hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3((n4 + 255) / 256), dim3(256), 0, s,
-                       (const float4 *)part, (float4 *)outf, n4, splits);
   return hipGetLastError();
 }
 
