@@ -81,44 +81,58 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const Tin *__restrict__ x,
   }
 }
 
-// grid: (rows); block: 256 threads.  Thread t owns rotation frequency i = t % (hd/2) for
-// every head it visits, so one sine/cosine pair per thread serves all its heads.
+// grid: (kv heads, sessions); block: 1024 threads.  One block rotates the session's tree
+// rows for one kv head and the G query heads that share it, so that its value columns
+// land as runs of consecutive slots in the head-dim-major value cache.  The rotation
+// table (one angle per tree row and frequency) is evaluated once per block.
+constexpr int ROPE_MAX_ROWS = 65, ROPE_MAX_HALF = 64, ROPE_THREADS = 1024;
 template <typename TW, typename TA>
-__global__ __launch_bounds__(256) void rope_kv_kernel(const float *__restrict__ qkv,
+__global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__restrict__ qkv,
                                                       TA *__restrict__ q_out, TreeMeta meta,
                                                       TW *__restrict__ ck, TW *__restrict__ cv,
                                                       int n1, int H, int Hkv, int hd,
                                                       int capacity,
                                                       const double *__restrict__ inv_freq) {
-  const int row = blockIdx.x, tid = threadIdx.x;
-  const int half = hd >> 1;
-  const int i = tid % half;
-  const int b = row / n1, r = row - b * n1;
-  const double ang = (double)meta.pos[row] * inv_freq[i];
-  double sd, cd;
-  sincos(ang, &sd, &cd);
-  const float c = (float)cd, s = (float)sd;
-  const float *base = qkv + (size_t)row * (H + 2 * Hkv) * hd;
-  TA *qo = q_out + (size_t)row * H * hd;
-  for (int p = tid; p < H * half; p += 256) {
-    const int h = p / half;
-    const float x1 = base[h * hd + i], x2 = base[h * hd + i + half];
-    qo[h * hd + i] = from_f32<TA>(x1 * c - x2 * s);
-    qo[h * hd + i + half] = from_f32<TA>(x2 * c + x1 * s);
+  __shared__ float cs[ROPE_MAX_ROWS * ROPE_MAX_HALF], sn[ROPE_MAX_ROWS * ROPE_MAX_HALF];
+  __shared__ float vs[ROPE_MAX_ROWS * (2 * ROPE_MAX_HALF + 1)];
+  const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int half = hd >> 1, G = H / Hkv;
+  const size_t W = (size_t)(H + 2 * Hkv) * hd;  // qkv row width
+  const float *base = qkv + (size_t)b * n1 * W;
+  for (int e = tid; e < n1 * half; e += ROPE_THREADS) {
+    const int r = e / half, i = e - r * half;
+    const double ang = (double)meta.pos[b * n1 + r] * inv_freq[i];
+    double sd, cd;
+    sincos(ang, &sd, &cd);
+    cs[e] = (float)cd;
+    sn[e] = (float)sd;
   }
-  const int slot = meta.sess_S[b] + r;
-  for (int p = tid; p < Hkv * half; p += 256) {
-    const int g = p / half;
-    const float *k = base + (H + g) * hd;
-    const float x1 = k[i], x2 = k[i + half];
-    const size_t kdst = (((size_t)b * Hkv + g) * capacity + slot) * hd;
+  for (int e = tid; e < n1 * hd; e += ROPE_THREADS) {  // this head's values, row-major
+    const int r = e / hd, dd = e - r * hd;
+    vs[r * (hd + 1) + dd] = base[r * W + (size_t)(H + Hkv + g) * hd + dd];
+  }
+  __syncthreads();
+  for (int e = tid; e < n1 * G * half; e += ROPE_THREADS) {  // queries
+    const int i = e % half, t = e / half, hh = t % G, r = t / G;
+    const int h = g * G + hh;
+    const float *x = base + r * W + (size_t)h * hd;
+    const float x1 = x[i], x2 = x[i + half], c = cs[r * half + i], s = sn[r * half + i];
+    TA *qo = q_out + ((size_t)b * n1 + r) * H * hd + (size_t)h * hd;
+    qo[i] = from_f32<TA>(x1 * c - x2 * s);
+    qo[i + half] = from_f32<TA>(x2 * c + x1 * s);
+  }
+  const int S = meta.sess_S[b];
+  for (int e = tid; e < n1 * half; e += ROPE_THREADS) {  // keys
+    const int i = e % half, r = e / half;
+    const float *k = base + r * W + (size_t)(H + g) * hd;
+    const float x1 = k[i], x2 = k[i + half], c = cs[e], s = sn[e];
+    const size_t kdst = (((size_t)b * Hkv + g) * capacity + S + r) * hd;
     ck[kdst + i] = from_f32<TW>(x1 * c - x2 * s);
     ck[kdst + i + half] = from_f32<TW>(x2 * c + x1 * s);
   }
-  for (int e = tid; e < Hkv * hd; e += 256) {   // values: head-dim-major cache
-    const int g = e / hd, dd = e - g * hd;
-    cv[(((size_t)b * Hkv + g) * hd + dd) * capacity + slot] =
-        from_f32<TW>(base[(H + Hkv) * hd + e]);
+  for (int e = tid; e < hd * n1; e += ROPE_THREADS) {  // values: consecutive threads, consecutive slots
+    const int dd = e / n1, r = e - dd * n1;
+    cv[(((size_t)b * Hkv + g) * hd + dd) * capacity + S + r] = from_f32<TW>(vs[r * (hd + 1) + dd]);
   }
 }
 
@@ -158,7 +172,9 @@ template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
                           int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s) {
-  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(B * n1), dim3(256),
+  if (n1 > ROPE_MAX_ROWS || hd > 2 * ROPE_MAX_HALF || H % Hkv) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(Hkv, B),
+                     dim3(ROPE_THREADS),
                      0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity,
                      inv_freq);
   return hipGetLastError();
