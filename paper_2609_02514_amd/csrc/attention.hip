@@ -162,8 +162,14 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     qi = qi < QR ? qi : QR - 1;
     const int r = qi / G, h = g * G + (qi - r * G);
     const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
+    // padding rows of the last tile multiply zeros (their outputs are dropped; zero
+    // operands keep the MFMA's switching, and so its power draw, down)
+    const bool pad = (wave + NW * t) * 16 + lr >= QR;
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) qf[t][s] = *(const f16x8 *)(qp + s * 32 + lg * 8);
+    for (int s = 0; s < KSTEPS; ++s) {
+      const f16x8 v = *(const f16x8 *)(qp + s * 32 + lg * 8);
+      qf[t][s] = pad ? f16x8{} : v;
+    }
     anc[t] = meta.anc[row0 + r];
     m_run[t] = -INFINITY;
     l_run[t] = 0.f;
