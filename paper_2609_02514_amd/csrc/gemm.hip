@@ -108,8 +108,10 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   const int lr = lane & 15, lk = lane >> 4;
 
   // DMA sources: block j of an operand covers tile rows ROWS_PER_BLK*j ..; lane l lands at
-  // row ROWS_PER_BLK*j + l / PIECES, physical piece l % PIECES.  Rows past M or N are
-  // clamped to the last row (their products are never stored).
+  // row ROWS_PER_BLK*j + l / PIECES, physical piece l % PIECES.  Rows of A past M get an
+  // offset past the end of A's buffer range, which the buffer load's range check turns
+  // into zeros (no fetch, and zero MFMA operands draw less power); rows of W past N are
+  // clamped to the last row.  Neither product is ever stored.
   const __amdgpu_buffer_rsrc_t rsa = make_rsrc(A, (uint32_t)((size_t)M * K * 2));
   const int wrows = EPI == acespec::EPI_SWIGLU ? 2 * N : N;
   const __amdgpu_buffer_rsrc_t rsb = make_rsrc(W, (uint32_t)((size_t)wrows * K * 2));
@@ -118,9 +120,9 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
 #pragma unroll
   for (int t = 0; t < A_DMA; ++t) {
     const int lrow = (w * A_DMA + t) * ROWS_PER_BLK + drow;
-    int r = m0 + lrow;
-    r = r < M ? r : M - 1;
-    va[t] = (uint32_t)r * K * 2 + (piece_off<ROWB>(lrow, dpc) - lrow * ROWB);
+    const int r = m0 + lrow;
+    va[t] = r < M ? (uint32_t)r * K * 2 + (piece_off<ROWB>(lrow, dpc) - lrow * ROWB)
+                  : (uint32_t)M * K * 2;
   }
 #pragma unroll
   for (int t = 0; t < B_DMA; ++t) {
