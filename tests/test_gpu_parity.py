@@ -174,6 +174,20 @@ def test_tail_exact_logit_ties():
     _run_tail(w, W=W)
 
 
+@pytest.mark.parametrize("T,top_p,top_k", [
+    (1.0, 1.0, 256),    # whole vocabulary in the nucleus, the largest payload
+    (0.05, 0.9, 1),     # near-greedy target, a one-token payload
+    (4.0, 0.3, 8),      # flat target, a nucleus of a small mass fraction
+    (0.8, 0.999, 200),  # nucleus boundary deep in the tail
+])
+def test_tail_parameter_extremes(T, top_p, top_k):
+    """Section III-B's sampling parameters at the ends of their ranges (temperature,
+    nucleus mass, payload size), on the same decisions as the other tail tests."""
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-extremes", d=256, V=5004, rows=64,
+                                          chain_len=4, top_k=top_k, T=T, top_p=top_p)
+    _run_tail(w)
+
+
 @pytest.mark.timeout(900)
 def test_tail_8b_full_size_sampled_rows():
     w = synth.get("8b-lmhead-tail")
