@@ -21,11 +21,15 @@
 // logit and the number of tied ids to keep (ids ascending).  The inverse CDFs run over
 // 256-id segments: segment masses are prefix-summed in LDS, and the chosen segment is
 // re-read and scanned across a wavefront.
+// Occupancy: 512 threads and 69 KB of LDS per row (the histograms and the segment tables
+// share storage), so two rows are in flight per CU and one row's scans and selections
+// overlap the other's passes over memory; each pass issues four loads per thread before
+// using any.
 #include "common.h"
 
 namespace {
 
-constexpr int VT = 1024;            // threads per row
+constexpr int VT = 512;             // threads per row (two rows in flight per CU)
 constexpr int NWV = VT / 64;        // waves
 constexpr int SEG = 256;            // ids per segment (one float4 per lane)
 constexpr int SEGMAX = 1024;        // vocab <= 262144
@@ -35,13 +39,21 @@ constexpr float LOG2E = 1.4426950408889634f;
 typedef unsigned long long u64;
 
 struct VSmem {
-  uint32_t cnt[4096];
-  u64 mass[4096];
-  uint32_t cntk[4096];
-  u64 seg_p[SEGMAX];       // per-segment mass of p_r, then its exclusive prefix
-  u64 seg_r[SEGMAX];       // same for the residual max(0, p_r - Q)
-  uint32_t tie_p[SEGMAX];  // per-segment count of ids tied at the top-p threshold (prefix)
-  uint32_t tie_k[SEGMAX];
+  // The threshold histograms (passes 1-3) and the per-segment tables (tie pass, pass 4)
+  // are never live together; sharing their storage keeps two rows in flight per CU.
+  union {
+    struct {
+      uint32_t cnt[4096];
+      u64 mass[4096];
+      uint32_t cntk[4096];
+    } h;
+    struct {
+      u64 seg_p[SEGMAX];       // per-segment mass of p_r, then its exclusive prefix
+      u64 seg_r[SEGMAX];       // same for the residual max(0, p_r - Q)
+      uint32_t tie_p[SEGMAX];  // per-segment count of ids tied at the top-p threshold (prefix)
+      uint32_t tie_k[SEGMAX];
+    } g;
+  };
   u64 wsum[NWV];
   uint32_t wsum32[NWV];
   float wmax[NWV];
@@ -114,7 +126,7 @@ AS_DEVICE void select_bin(VSmem &sm, const uint32_t *cnt, const u64 *mass, int n
     if (MASS) { sm.sel_p = 0; sm.above_p = base; }
     else { sm.sel_k = 0; sm.above_k = (uint32_t)base; }
   }
-  const int per = nb / VT > 0 ? nb / VT : 1;   // bins per thread (4 or 1)
+  const int per = nb / VT > 0 ? nb / VT : 1;   // bins per thread
   const bool owner = t * per < nb;
   u64 local = 0;
   if (owner) {
@@ -222,7 +234,7 @@ AS_DEVICE int seg_inverse_cdf(const float *z, const float *q, int V, int s, u64 
   uint32_t key[4], rank[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) key[i] = f32_key(zz[i]);
-  if (sel.c_p > 1) tie_ranks(key, valid, sel.tau_p, sm.tie_p[s], rank);
+  if (sel.c_p > 1) tie_ranks(key, valid, sel.tau_p, sm.g.tie_p[s], rank);
   else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) rank[i] = 0;
@@ -263,6 +275,19 @@ AS_DEVICE int find_segment(const u64 *excl, int nseg, u64 target) {
   return lo;
 }
 
+// Loads the VU float4 this thread handles in one step of a pass over the row (-inf past
+// the end), all issued before any is used: one load in flight per thread leaves the
+// passes bound by memory latency rather than bandwidth.
+constexpr int VU = 4;
+AS_DEVICE void load_step(const float *z, int V, int i0, float4 (&v)[VU]) {
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    const int i = i0 + u * VT * 4;
+    v[u] = i < V ? *(const float4 *)(z + i)
+                 : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+  }
+}
+
 __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) {
   __shared__ VSmem sm;
   const int row = blockIdx.x;
@@ -273,9 +298,12 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
 
   // ---- pass 0: row max -----------------------------------------------------------
   float mx = -INFINITY;
-  for (int i = tid * 4; i < V; i += VT * 4) {
-    const float4 v = *(const float4 *)(z + i);
-    mx = fmaxf(fmaxf(mx, fmaxf(v.x, v.y)), fmaxf(v.z, v.w));
+  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
+    float4 vv[VU];
+    load_step(z, V, i0, vv);
+#pragma unroll
+    for (int u = 0; u < VU; ++u)
+      mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
   }
   Sel sel;
   sel.M = block_max(mx, sm);
@@ -283,23 +311,28 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
 
   // ---- pass 1: total mass, 12-bit histograms ---------------------------------------
   for (int i = tid; i < 4096; i += VT) {
-    sm.cnt[i] = 0;
-    sm.mass[i] = 0;
-    sm.cntk[i] = 0;
+    sm.h.cnt[i] = 0;
+    sm.h.mass[i] = 0;
+    sm.h.cntk[i] = 0;
   }
   if (tid == 0) sm.ncand = 0;
   __syncthreads();
   u64 tot = 0;
-  for (int i = tid * 4; i < V; i += VT * 4) {
-    const float4 v = *(const float4 *)(z + i);
-    const float zz[4] = {v.x, v.y, v.z, v.w};
+  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
+    float4 vv[VU];
+    load_step(z, V, i0, vv);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t key = f32_key(zz[j]);
-      const u64 w = fixw(elem_e(zz[j], sel));
-      tot += w;
-      atomicAdd(&sm.cnt[key >> 20], 1u);
-      atomicAdd(&sm.mass[key >> 20], w);
+    for (int u = 0; u < VU; ++u) {
+      if (i0 + u * VT * 4 >= V) break;
+      const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t key = f32_key(zz[j]);
+        const u64 w = fixw(elem_e(zz[j], sel));
+        tot += w;
+        atomicAdd(&sm.h.cnt[key >> 20], 1u);
+        atomicAdd(&sm.h.mass[key >> 20], w);
+      }
     }
   }
   const u64 S_fx = block_sum(tot, sm);  // includes a barrier after the histogram writes
@@ -311,71 +344,81 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
 
   int bp, bk;
   u64 ap, ak;
-  select_bin<true>(sm, sm.cnt, sm.mass, 4096, T_p, 0, bp, ap);
-  select_bin<false>(sm, sm.cnt, sm.mass, 4096, K, 0, bk, ak);
+  select_bin<true>(sm, sm.h.cnt, sm.h.mass, 4096, T_p, 0, bp, ap);
+  select_bin<false>(sm, sm.h.cnt, sm.h.mass, 4096, K, 0, bk, ak);
 
   // ---- pass 2: refine bits 19..8 inside the selected bins ------------------------------
   for (int i = tid; i < 4096; i += VT) {
-    sm.cnt[i] = 0;
-    sm.mass[i] = 0;
-    sm.cntk[i] = 0;
+    sm.h.cnt[i] = 0;
+    sm.h.mass[i] = 0;
+    sm.h.cntk[i] = 0;
   }
   __syncthreads();
-  for (int i = tid * 4; i < V; i += VT * 4) {
-    const float4 v = *(const float4 *)(z + i);
-    const float zz[4] = {v.x, v.y, v.z, v.w};
+  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
+    float4 vv[VU];
+    load_step(z, V, i0, vv);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t key = f32_key(zz[j]);
-      const int hi = key >> 20, mid = (key >> 8) & 0xFFF;
-      if (hi == bp) {
-        atomicAdd(&sm.cnt[mid], 1u);
-        atomicAdd(&sm.mass[mid], fixw(elem_e(zz[j], sel)));
+    for (int u = 0; u < VU; ++u) {
+      if (i0 + u * VT * 4 >= V) break;
+      const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t key = f32_key(zz[j]);
+        const int hi = key >> 20, mid = (key >> 8) & 0xFFF;
+        if (hi == bp) {
+          atomicAdd(&sm.h.cnt[mid], 1u);
+          atomicAdd(&sm.h.mass[mid], fixw(elem_e(zz[j], sel)));
+        }
+        if (hi == bk) atomicAdd(&sm.h.cntk[mid], 1u);
       }
-      if (hi == bk) atomicAdd(&sm.cntk[mid], 1u);
     }
   }
   __syncthreads();
   int sp, sk;
   u64 ap2, ak2;
-  select_bin<true>(sm, sm.cnt, sm.mass, 4096, T_p, ap, sp, ap2);
-  select_bin<false>(sm, sm.cntk, sm.mass, 4096, K, ak, sk, ak2);
+  select_bin<true>(sm, sm.h.cnt, sm.h.mass, 4096, T_p, ap, sp, ap2);
+  select_bin<false>(sm, sm.h.cntk, sm.h.mass, 4096, K, ak, sk, ak2);
   const uint32_t pre_p = ((uint32_t)bp << 12) | (uint32_t)sp;
   const uint32_t pre_k = ((uint32_t)bk << 12) | (uint32_t)sk;
 
   // ---- pass 3: refine bits 7..0 ------------------------------------------------------
   for (int i = tid; i < 256; i += VT) {
-    sm.cnt[i] = 0;
-    sm.mass[i] = 0;
-    sm.cntk[i] = 0;
+    sm.h.cnt[i] = 0;
+    sm.h.mass[i] = 0;
+    sm.h.cntk[i] = 0;
   }
   __syncthreads();
-  for (int i = tid * 4; i < V; i += VT * 4) {
-    const float4 v = *(const float4 *)(z + i);
-    const float zz[4] = {v.x, v.y, v.z, v.w};
+  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
+    float4 vv[VU];
+    load_step(z, V, i0, vv);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t key = f32_key(zz[j]);
-      if ((key >> 8) == pre_p) {
-        atomicAdd(&sm.cnt[key & 0xFF], 1u);
-        atomicAdd(&sm.mass[key & 0xFF], fixw(elem_e(zz[j], sel)));
+    for (int u = 0; u < VU; ++u) {
+      if (i0 + u * VT * 4 >= V) break;
+      const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t key = f32_key(zz[j]);
+        if ((key >> 8) == pre_p) {
+          atomicAdd(&sm.h.cnt[key & 0xFF], 1u);
+          atomicAdd(&sm.h.mass[key & 0xFF], fixw(elem_e(zz[j], sel)));
+        }
+        if ((key >> 8) == pre_k) atomicAdd(&sm.h.cntk[key & 0xFF], 1u);
       }
-      if ((key >> 8) == pre_k) atomicAdd(&sm.cntk[key & 0xFF], 1u);
     }
   }
   __syncthreads();
   int lp, lk;
   u64 ap3, ak3;
-  select_bin<true>(sm, sm.cnt, sm.mass, 256, T_p, ap2, lp, ap3);
-  select_bin<false>(sm, sm.cntk, sm.mass, 256, K, ak2, lk, ak3);
+  select_bin<true>(sm, sm.h.cnt, sm.h.mass, 256, T_p, ap2, lp, ap3);
+  select_bin<false>(sm, sm.h.cntk, sm.h.mass, 256, K, ak2, lk, ak3);
   sel.tau_p = (pre_p << 8) | (uint32_t)lp;
   sel.tau_k = (pre_k << 8) | (uint32_t)lk;
-  sel.c_p = sm.cnt[lp];
-  sel.c_k = sm.cntk[lk];
+  sel.c_p = sm.h.cnt[lp];
+  sel.c_k = sm.h.cntk[lk];
   sel.above_p = ap3;
   sel.above_k = (uint32_t)ak3;
   {
-    const u64 w_tau = sm.mass[lp] / (sel.c_p ? sel.c_p : 1);
+    const u64 w_tau = sm.h.mass[lp] / (sel.c_p ? sel.c_p : 1);
     const u64 need = T_p - ap3;  // > 0
     u64 j = w_tau ? (need + w_tau - 1) / w_tau : 1;
     if (j < 1) j = 1;
@@ -406,17 +449,17 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
       np = (uint32_t)wave_sum_i32((int)np);
       nk = (uint32_t)wave_sum_i32((int)nk);
       if (lane == 0) {
-        sm.tie_p[s] = np;
-        sm.tie_k[s] = nk;
+        sm.g.tie_p[s] = np;
+        sm.g.tie_k[s] = nk;
       }
     }
     __syncthreads();
     if (tid == 0) {  // exclusive prefixes over segments (sequential: rare path)
       uint32_t rp = 0, rk = 0;
       for (int s = 0; s < nseg; ++s) {
-        const uint32_t a0 = sm.tie_p[s], b0 = sm.tie_k[s];
-        sm.tie_p[s] = rp;
-        sm.tie_k[s] = rk;
+        const uint32_t a0 = sm.g.tie_p[s], b0 = sm.g.tie_k[s];
+        sm.g.tie_p[s] = rp;
+        sm.g.tie_k[s] = rk;
         rp += a0;
         rk += b0;
       }
@@ -438,26 +481,37 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   const bool dense_q = a.q_scalar == nullptr;
   const bool resid = has_child && dense_q;
   const float *q = dense_q ? a.q + (size_t)row * V : nullptr;
-  for (int s = wave; s < nseg; s += NWV) {
+  for (int s0 = wave; s0 < nseg; s0 += NWV * VU) {
+  // the VU segments of this step are loaded before any is used
+  float4 z4u[VU], q4u[VU];
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    const int id0 = (s0 + u * NWV) * SEG + lane * 4;
+    z4u[u] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    q4u[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (s0 + u * NWV < nseg && id0 < V) {
+      z4u[u] = *(const float4 *)(z + id0);
+      if (resid) q4u[u] = *(const float4 *)(q + id0);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    const int s = s0 + u * NWV;
+    if (s >= nseg) break;
     const int id0 = s * SEG + lane * 4;
     const bool valid = id0 < V;
-    float4 z4 = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-    float4 q4 = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (valid) {
-      z4 = *(const float4 *)(z + id0);
-      if (resid) q4 = *(const float4 *)(q + id0);
-    }
+    const float4 z4 = z4u[u], q4 = q4u[u];
     const float zz[4] = {z4.x, z4.y, z4.z, z4.w};
     const float qq[4] = {q4.x, q4.y, q4.z, q4.w};
     uint32_t key[4], rp[4], rk[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) key[j] = f32_key(zz[j]);
-    if (sel.c_p > 1) tie_ranks(key, valid, sel.tau_p, sm.tie_p[s], rp);
+    if (sel.c_p > 1) tie_ranks(key, valid, sel.tau_p, sm.g.tie_p[s], rp);
     else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) rp[j] = 0;
     }
-    if (sel.c_k > 1) tie_ranks(key, valid, sel.tau_k, sm.tie_k[s], rk);
+    if (sel.c_k > 1) tie_ranks(key, valid, sel.tau_k, sm.g.tie_k[s], rk);
     else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) rk[j] = 0;
@@ -482,21 +536,36 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     sp_ = wave_sum_u64(sp_);
     sr_ = wave_sum_u64(sr_);
     if (lane == 0) {
-      sm.seg_p[s] = sp_;
-      sm.seg_r[s] = sr_;
+      sm.g.seg_p[s] = sp_;
+      sm.g.seg_r[s] = sr_;
     }
+  }
   }
   __syncthreads();
   // exclusive prefixes over segments
   u64 Ptot, Rtot;
   {
-    const u64 vp = tid < nseg ? sm.seg_p[tid] : 0;
-    const u64 vr = tid < nseg ? sm.seg_r[tid] : 0;
-    const u64 ep = block_scan_excl(vp, sm, Ptot);
-    const u64 er = block_scan_excl(vr, sm, Rtot);
-    if (tid < nseg) {
-      sm.seg_p[tid] = ep;
-      sm.seg_r[tid] = er;
+    constexpr int SPT = SEGMAX / VT;  // consecutive segments per thread
+    u64 lp[SPT], lr[SPT], vp = 0, vr = 0;
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+      const int sg = tid * SPT + j;
+      lp[j] = sg < nseg ? sm.g.seg_p[sg] : 0;
+      lr[j] = sg < nseg ? sm.g.seg_r[sg] : 0;
+      vp += lp[j];
+      vr += lr[j];
+    }
+    u64 ep = block_scan_excl(vp, sm, Ptot);
+    u64 er = block_scan_excl(vr, sm, Rtot);
+#pragma unroll
+    for (int j = 0; j < SPT; ++j) {
+      const int sg = tid * SPT + j;
+      if (sg < nseg) {
+        sm.g.seg_p[sg] = ep;
+        sm.g.seg_r[sg] = er;
+      }
+      ep += lp[j];
+      er += lr[j];
     }
   }
   __syncthreads();
@@ -528,8 +597,8 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     int id = -1;
     if (dense_q) {
       const u64 target = (u64)floor((double)u[(size_t)row * 3 + 2] * (double)Ptot);
-      const int sg = find_segment(sm.seg_p, nseg, target);
-      id = seg_inverse_cdf(z, q, V, sg, sm.seg_p[sg], target, 0, sel, sm);
+      const int sg = find_segment(sm.g.seg_p, nseg, target);
+      id = seg_inverse_cdf(z, q, V, sg, sm.g.seg_p[sg], target, 0, sel, sm);
     }
     if (lane == 0) a.bonus[row] = id;
   }
@@ -539,7 +608,7 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     a.accept[row] = 1;
     a.resample[row] = -1;
   }
-  // Waves 1..15 take the children in order (wave 0 drew the bonus).
+  // Waves 1.. take the children in turn (wave 0 drew the bonus).
   if (has_child && wave >= 1) {
     int seen = 0;
     const int c_lo = tail ? 0 : r + 1, c_hi = tail ? 1 : a.n1;
@@ -567,7 +636,7 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
         const float4 z4 = valid ? *(const float4 *)(z + id0) : make_float4(0.f, 0.f, 0.f, 0.f);
         const uint32_t keys[4] = {f32_key(z4.x), f32_key(z4.y), f32_key(z4.z), f32_key(z4.w)};
         uint32_t rk4[4];
-        tie_ranks(keys, valid, sel.tau_p, sm.tie_p[sx], rk4);
+        tie_ranks(keys, valid, sel.tau_p, sm.g.tie_p[sx], rk4);
         const int src = (x - sx * SEG) >> 2;
         const uint32_t mine_rank = rk4[0] * ((x & 3) == 0) + rk4[1] * ((x & 3) == 1) +
                                    rk4[2] * ((x & 3) == 2) + rk4[3] * ((x & 3) == 3);
@@ -582,12 +651,12 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
         // no cloud-side resampling in the scalar protocol
       } else if (Rtot > 0) {
         const u64 target = (u64)floor((double)u1 * (double)Rtot);
-        const int sg = find_segment(sm.seg_r, nseg, target);
-        res = seg_inverse_cdf(z, q, V, sg, sm.seg_r[sg], target, 1, sel, sm);
+        const int sg = find_segment(sm.g.seg_r, nseg, target);
+        res = seg_inverse_cdf(z, q, V, sg, sm.g.seg_r[sg], target, 1, sel, sm);
       } else {
         const u64 target = (u64)floor((double)u1 * (double)Ptot);
-        const int sg = find_segment(sm.seg_p, nseg, target);
-        res = seg_inverse_cdf(z, q, V, sg, sm.seg_p[sg], target, 0, sel, sm);
+        const int sg = find_segment(sm.g.seg_p, nseg, target);
+        res = seg_inverse_cdf(z, q, V, sg, sm.g.seg_p[sg], target, 0, sel, sm);
       }
       if (lane == 0) {
         a.accept[child] = acc ? 1 : 0;
