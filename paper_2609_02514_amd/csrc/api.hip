@@ -148,12 +148,15 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
                                stream));
   RUN(K_EMBED, launch_embed<T>((const T *)w->embed, meta.tok, ctx->x, R, D, stream));
   const size_t layer_stride = (size_t)B * Hkv * cap * hd;
+  // The residual projections (O, down) also apply the RMSNorm that opens the next block
+  // (the MLP's, the next layer's attention norm, the final norm).
+  RUN(K_RMSNORM, (launch_rmsnorm<T, float>(
+                     ctx->x, (const T *)(L > 0 ? w->layers[0].attn_norm : w->final_norm), x_a,
+                     R, D, d.rms_eps, stream)));
   for (int l = 0; l < L; ++l) {
     const acespec_layer_weights &lw = w->layers[l];
     T *ck = (T *)kv->k + l * layer_stride;
     T *cv = (T *)kv->v + l * layer_stride;
-    RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.attn_norm, x_a, R, D,
-                                             d.rms_eps, stream)));
     RUN(K_GEMM_QKV, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)lw.wqkv, R, QKVN, D, nullptr,
                                        ctx->qkv, aux, stream)));
     RUN(K_ROPE, launch_rope_kv<T>(ctx->qkv, x_q, meta, ck, cv, B, n1, H, Hkv, hd, cap,
@@ -162,17 +165,15 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
     RUN(K_ATTN, launch_attention<T>(x_q, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
                                     ctx->part_cap, B, n1, H, Hkv, hd, cap, ctx->cus, stream,
                                     &nsplit));
-    RUN(K_GEMM_O, (launch_gemm<T, A>(EPI_RESID, x_attn, (const T *)lw.wo, R, D, H * hd, nullptr,
-                                     ctx->x, aux, stream)));
-    RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)lw.mlp_norm, x_a, R, D,
-                                             d.rms_eps, stream)));
+    RUN(K_GEMM_O, (launch_gemm_resid_norm<T, A>(x_attn, (const T *)lw.wo, R, D, H * hd, ctx->x,
+                                                (const T *)lw.mlp_norm, x_a, d.rms_eps, aux,
+                                                stream)));
     RUN(K_GEMM_GATE_UP, (launch_gemm<T, A>(EPI_SWIGLU, x_a, (const T *)lw.w_gate_up, R, F, D,
                                            x_h, nullptr, aux, stream)));
-    RUN(K_GEMM_DOWN, (launch_gemm<T, A>(EPI_RESID, x_h, (const T *)lw.w_down, R, D, F, nullptr,
-                                        ctx->x, aux, stream)));
+    const T *next_norm = (const T *)(l + 1 < L ? w->layers[l + 1].attn_norm : w->final_norm);
+    RUN(K_GEMM_DOWN, (launch_gemm_resid_norm<T, A>(x_h, (const T *)lw.w_down, R, D, F, ctx->x,
+                                                   next_norm, x_a, d.rms_eps, aux, stream)));
   }
-  RUN(K_RMSNORM, (launch_rmsnorm<T, float>(ctx->x, (const T *)w->final_norm, x_a, R, D,
-                                           d.rms_eps, stream)));
   RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr,
                                     logits, aux, stream)));
   VocabArgs va;

@@ -177,6 +177,16 @@ hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
                        typename ActOf<TW>::type *out, float *outf, const GemmAux &aux,
                        hipStream_t s);
 
+// x[M, N] += A . W^T followed by out = RMSNorm(x) * gain (the residual projection and the
+// norm that opens the next block).  When the product is sliced along K in every tile the
+// slices are summed, added to x and normalised by one row-wise kernel (x is read and
+// written once); otherwise the product's own epilogue adds to x and a separate RMSNorm
+// follows.  Results are identical either way.
+template <typename TW, typename TA>
+hipError_t launch_gemm_resid_norm(const TA *A, const TW *W, int M, int N, int K, float *x,
+                                  const TW *gain, typename ActOf<TW>::type *out, float eps,
+                                  const GemmAux &aux, hipStream_t s);
+
 // The fp16-activation MFMA GEMM (weights TB = bf16, widened to fp16 in registers) with
 // an explicit tiling (var >= 0) and split count (splits_override > 0); var < 0 /
 // splits_override <= 0 choose automatically.

@@ -310,6 +310,62 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
   }
 }
 
+// Residual projection fixup fused with the following RMSNorm: one 256-thread block per
+// row sums the row's k-slices (every tile sliced), adds them to the fp32 residual x,
+// writes x back and emits RMSNorm(x) * gain.  Thread t owns the float4 columns
+// t, t + 256, ... (at most 8, N <= 8192) in the same order as the RMSNorm kernel, so the
+// result is bit-identical to the unfused path.
+template <typename TG, int TBM, int TBN>
+__global__ __launch_bounds__(256) void fixup_resid_norm_kernel(
+    const float *__restrict__ part, float *__restrict__ x, const TG *__restrict__ gain,
+    f16 *__restrict__ out, int N, int mt, int tsplit, float eps) {
+  constexpr int MAXJ = 8;
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const int tm = row / TBM, lrow = row - tm * TBM;
+  const int n4 = N >> 2;
+  float4 v[MAXJ];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    const int c = tid + 256 * j;
+    if (c < n4) {
+      const int col = 4 * c, tn = col / TBN, tc = col - tn * TBN;
+      const float *pt = part + (size_t)(tn * mt + tm) * tsplit * (TBM * TBN) +
+                        (size_t)lrow * TBN + tc;
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int sp = 0; sp < tsplit; ++sp) {
+        const float4 w = *(const float4 *)(pt + (size_t)sp * (TBM * TBN));
+        a.x += w.x; a.y += w.y; a.z += w.z; a.w += w.w;
+      }
+      float4 *xp = (float4 *)(x + (size_t)row * N) + c;
+      float4 t = *xp;
+      t.x += a.x; t.y += a.y; t.z += a.z; t.w += a.w;
+      *xp = t;
+      v[j] = t;
+      ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+    }
+  }
+  __shared__ float red[4];
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float scale = 1.0f / sqrtf(tot / (float)N + eps);
+  f16 *o = out + (size_t)row * N;
+#pragma unroll
+  for (int j = 0; j < MAXJ; ++j) {
+    const int c = tid + 256 * j;
+    if (c < n4) {
+      float g[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) g[e] = (float)gain[4 * c + e];
+      typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+      *(h4 *)(o + 4 * c) = h4{(f16)(v[j].x * scale * g[0]), (f16)(v[j].y * scale * g[1]),
+                              (f16)(v[j].z * scale * g[2]), (f16)(v[j].w * scale * g[3])};
+    }
+  }
+}
+
 // ------------------------------------------------------------------------------------
 // fp32 reference-precision path (tiny models): 64 x 64 tiles, 4 x 4 outputs per thread.
 // ------------------------------------------------------------------------------------
@@ -521,6 +577,50 @@ hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 
   return hipGetLastError();
 }
 
+template <int V, typename TB>
+void launch_resid_norm_fixup(hipStream_t s, const float *part, float *x, const TB *gain,
+                             f16 *out, int M, int N, int mt, int tsplit, float eps) {
+  constexpr GemmVariant v = kVariants[V];
+  constexpr int TBM = v.wmn * v.wtm * 16, TBN = v.wnn * v.wtn * 16;
+  hipLaunchKernelGGL((fixup_resid_norm_kernel<TB, TBM, TBN>), dim3(M), dim3(256), 0, s, part,
+                     x, gain, out, N, mt, tsplit, eps);
+}
+
+template <>
+hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
+                                             float *x, const bf16 *gain, f16 *out, float eps,
+                                             const GemmAux &aux, hipStream_t s) {
+  const int var = pick_variant(EPI_RESID, M, N, K);
+  const GemmVariant v = kVariants[var];
+  const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
+  const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
+  const SplitPlan sp =
+      plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  if (sp.full != 0 || sp.tsplit < 2 || N % tbn != 0 || N > 8 * 4 * 256) {
+    hipError_t e = launch_f16w_variant<bf16>(var, 0, EPI_RESID, A, W, M, N, K, nullptr, x,
+                                             aux.part, aux.part_cap, aux.cus, s);
+    if (e != hipSuccess) return e;
+    return launch_rmsnorm<bf16, float>(x, gain, out, M, N, eps, s);
+  }
+  // every tile sliced: the GEMM writes only partials, the row kernel does the rest
+  switch (var) {
+#define CASE(VV)                                                                            \
+  case VV: {                                                                                \
+    constexpr GemmVariant g = kVariants[VV];                                                \
+    hipLaunchKernelGGL(                                                                     \
+        (gemm_f16w_kernel<EPI_RESID, bf16, g.wmn, g.wnn, g.wtm, g.wtn, g.nst, g.occ, g.kss>), \
+        dim3(mt * nt * sp.tsplit), dim3(g.wmn * g.wnn * 64), 0, s, A, W, M, N, K, nullptr,   \
+        x, aux.part, mt, nt, 0, sp.tsplit);                                                 \
+    launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
+    break;                                                                                  \
+  }
+    CASE(0) CASE(1) CASE(2) CASE(3)
+#undef CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template hipError_t launch_f16w_variant<bf16>(int, int, int, const f16 *, const bf16 *, int, int,
                                               int, f16 *, float *, float *, long long, int,
                                               hipStream_t);
@@ -555,6 +655,15 @@ hipError_t launch_gemm<float, float>(int epi, const float *A, const float *W, in
                          outf);
   }
   return hipGetLastError();
+}
+
+template <>
+hipError_t launch_gemm_resid_norm<float, float>(const float *A, const float *W, int M, int N,
+                                                int K, float *x, const float *gain, float *out,
+                                                float eps, const GemmAux &aux, hipStream_t s) {
+  hipError_t e = launch_gemm<float, float>(EPI_RESID, A, W, M, N, K, nullptr, x, aux, s);
+  if (e != hipSuccess) return e;
+  return launch_rmsnorm<float, float>(x, gain, out, M, N, eps, s);
 }
 
 }  // namespace acespec
