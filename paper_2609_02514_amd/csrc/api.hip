@@ -59,6 +59,7 @@ struct acespec_ctx {
   long long gpart_cap = 0;
   int cus = 256;
   double *inv_freq = nullptr;
+  float2 *rot = nullptr;      // RoPE (cos, sin) per tree row and frequency, per step
   TreeMeta meta{};
   // timing
   bool timing = false;
@@ -147,6 +148,7 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   RUN(K_TREE, launch_tree_prep(tokens, parents, kv->prefix_len, B, n1, V, cap, meta, o->status,
                                stream));
   RUN(K_EMBED, launch_embed<T>((const T *)w->embed, meta.tok, ctx->x, R, D, stream));
+  if (L > 0) RUN(K_ROPE, launch_rope_table(meta.pos, ctx->inv_freq, ctx->rot, R, hd / 2, stream));
   const size_t layer_stride = (size_t)B * Hkv * cap * hd;
   // The residual projections (O, down) also apply the RMSNorm that opens the next block
   // (the MLP's, the next layer's attention norm, the final norm).
@@ -157,10 +159,9 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
     const acespec_layer_weights &lw = w->layers[l];
     T *ck = (T *)kv->k + l * layer_stride;
     T *cv = (T *)kv->v + l * layer_stride;
-    RUN(K_GEMM_QKV, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)lw.wqkv, R, QKVN, D, nullptr,
-                                       ctx->qkv, aux, stream)));
-    RUN(K_ROPE, launch_rope_kv<T>(ctx->qkv, x_q, meta, ck, cv, B, n1, H, Hkv, hd, cap,
-                                  ctx->inv_freq, stream));
+    const RopeOut<T> ro{x_q, ck, cv, ctx->rot, meta.sess_S, n1, H, Hkv, hd, cap};
+    RUN(K_GEMM_QKV, (launch_qkv_rope<T, A>(x_a, (const T *)lw.wqkv, R, QKVN, D, ctx->qkv, ro,
+                                           meta, B, aux, stream)));
     int nsplit = 1;
     RUN(K_ATTN, launch_attention<T>(x_q, ck, cv, meta, x_attn, ctx->part_o, ctx->part_ml,
                                     ctx->part_cap, B, n1, H, Hkv, hd, cap, ctx->cus, stream,
@@ -300,7 +301,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
-  void *p_qkv = nullptr, *p_gpart = nullptr;
+  void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
@@ -314,6 +315,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       {(size_t)c->part_cap * 4, &p_po},
       {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
       {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
+      {layers ? R * (size_t)d.head_dim / 2 * 8 : 0, &p_rot},
       {(size_t)8 * R * d.d_model * 4, &p_gpart},
       {R * 4, &p_tok}, {R * 4, &p_par}, {R * 4, &p_pos}, {R * 4, &p_depth}, {R * 8, &p_anc},
       {(size_t)max_batch * 4, &p_S}};
@@ -343,6 +345,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_o = (float *)p_po;
   c->part_ml = (float *)p_pml;
   c->inv_freq = (double *)p_if;
+  c->rot = (float2 *)p_rot;
   c->meta.tok = (int32_t *)p_tok;
   c->meta.par = (int32_t *)p_par;
   c->meta.pos = (int32_t *)p_pos;

@@ -153,18 +153,25 @@ hipError_t launch_rmsnorm(const TIN *x, const TW *gain, typename ActOf<TW>::type
 // RoPE on q and k of the fp32 QKV projection; q goes to q_out (activation type,
 // [rows, H*hd]), k and v to the cache slots of the tree rows (keys [B][Hkv][cap][hd],
 // values head-dim-major [B][Hkv][hd][cap]).
+// rot[row * hd/2 + i] = (cos, sin) of pos[row] * inv_freq[i], evaluated in double and
+// rounded to fp32 (positions are fixed for the whole step, so one table serves all layers).
+hipError_t launch_rope_table(const int32_t *pos, const double *inv_freq, float2 *rot, int rows,
+                             int half, hipStream_t s);
 template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
-                          int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s);
+                          int Hkv, int hd, int capacity, const float2 *rot, hipStream_t s);
 
-enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3 };
+
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3, EPI_QKV_ROPE = 4 };
 
 // C[M, N] = A[M, K] . W[N, K]^T with the epilogue:
 //  EPI_STORE : out (activation type) [M, N]
 //  EPI_RESID : resid (fp32) [M, N] += C
 //  EPI_SWIGLU: W holds 2F rows (gate, up); out[M, F] = silu(gate) * up, N = F
 //  EPI_F32   : outf (fp32) [M, N] = C
+//  EPI_QKV_ROPE: C is the QKV projection; RoPE, rounding and the cache write of the tree
+//              rows happen in the epilogue (see launch_qkv_rope)
 // A is in the activation type.  aux.part: fp32 workspace for split-K partials
 // (aux.part_cap floats), aux.cus: compute units of the device.
 struct GemmAux {
@@ -172,6 +179,23 @@ struct GemmAux {
   long long part_cap;
   int cus;
 };
+// Where the QKV projection's RoPE epilogue puts its results: rotated queries (activation
+// type, [rows, H*hd]) and the tree rows' keys and values in their cache slots.
+template <typename TW> struct RopeOut {
+  typename ActOf<TW>::type *q;
+  TW *ck, *cv;
+  const float2 *rot;
+  const int32_t *sess_S;
+  int n1, H, Hkv, hd, capacity;
+};
+// The QKV projection with RoPE and the cache write fused into its epilogue when the
+// product is not sliced along K; otherwise the fp32 projection goes to qkv and the RoPE
+// kernel follows.  Results are identical either way.
+template <typename TW, typename TA>
+hipError_t launch_qkv_rope(const TA *A, const TW *W, int M, int N, int K, float *qkv,
+                           const RopeOut<TW> &ro, const TreeMeta &meta, int B,
+                           const GemmAux &aux, hipStream_t s);
+
 template <typename TW, typename TA>
 hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
                        typename ActOf<TW>::type *out, float *outf, const GemmAux &aux,

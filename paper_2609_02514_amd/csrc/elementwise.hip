@@ -81,10 +81,20 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const Tin *__restrict__ x,
   }
 }
 
+__global__ void rope_table_kernel(const int32_t *__restrict__ pos,
+                                  const double *__restrict__ inv_freq, float2 *__restrict__ rot,
+                                  int rows, int half) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= rows * half) return;
+  const int row = idx / half, i = idx - row * half;
+  double sd, cd;
+  sincos((double)pos[row] * inv_freq[i], &sd, &cd);
+  rot[idx] = make_float2((float)cd, (float)sd);
+}
+
 // grid: (kv heads, sessions); block: 1024 threads.  One block rotates the session's tree
 // rows for one kv head and the G query heads that share it, so that its value columns
-// land as runs of consecutive slots in the head-dim-major value cache.  The rotation
-// table (one angle per tree row and frequency) is evaluated once per block.
+// land as runs of consecutive slots in the head-dim-major value cache.
 constexpr int ROPE_MAX_ROWS = 65, ROPE_MAX_HALF = 64, ROPE_THREADS = 1024;
 template <typename TW, typename TA>
 __global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__restrict__ qkv,
@@ -92,21 +102,13 @@ __global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__re
                                                       TW *__restrict__ ck, TW *__restrict__ cv,
                                                       int n1, int H, int Hkv, int hd,
                                                       int capacity,
-                                                      const double *__restrict__ inv_freq) {
-  __shared__ float cs[ROPE_MAX_ROWS * ROPE_MAX_HALF], sn[ROPE_MAX_ROWS * ROPE_MAX_HALF];
+                                                      const float2 *__restrict__ rot) {
   __shared__ float vs[ROPE_MAX_ROWS * (2 * ROPE_MAX_HALF + 1)];
   const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int half = hd >> 1, G = H / Hkv;
   const size_t W = (size_t)(H + 2 * Hkv) * hd;  // qkv row width
   const float *base = qkv + (size_t)b * n1 * W;
-  for (int e = tid; e < n1 * half; e += ROPE_THREADS) {
-    const int r = e / half, i = e - r * half;
-    const double ang = (double)meta.pos[b * n1 + r] * inv_freq[i];
-    double sd, cd;
-    sincos(ang, &sd, &cd);
-    cs[e] = (float)cd;
-    sn[e] = (float)sd;
-  }
+  const float2 *rt = rot + (size_t)b * n1 * half;
   for (int e = tid; e < n1 * hd; e += ROPE_THREADS) {  // this head's values, row-major
     const int r = e / hd, dd = e - r * hd;
     vs[r * (hd + 1) + dd] = base[r * W + (size_t)(H + Hkv + g) * hd + dd];
@@ -116,19 +118,21 @@ __global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__re
     const int i = e % half, t = e / half, hh = t % G, r = t / G;
     const int h = g * G + hh;
     const float *x = base + r * W + (size_t)h * hd;
-    const float x1 = x[i], x2 = x[i + half], c = cs[r * half + i], s = sn[r * half + i];
+    const float2 cs = rt[r * half + i];
+    const float x1 = x[i], x2 = x[i + half];
     TA *qo = q_out + ((size_t)b * n1 + r) * H * hd + (size_t)h * hd;
-    qo[i] = from_f32<TA>(x1 * c - x2 * s);
-    qo[i + half] = from_f32<TA>(x2 * c + x1 * s);
+    qo[i] = from_f32<TA>(x1 * cs.x - x2 * cs.y);
+    qo[i + half] = from_f32<TA>(x2 * cs.x + x1 * cs.y);
   }
   const int S = meta.sess_S[b];
   for (int e = tid; e < n1 * half; e += ROPE_THREADS) {  // keys
     const int i = e % half, r = e / half;
     const float *k = base + r * W + (size_t)(H + g) * hd;
-    const float x1 = k[i], x2 = k[i + half], c = cs[e], s = sn[e];
+    const float2 cs = rt[e];
+    const float x1 = k[i], x2 = k[i + half];
     const size_t kdst = (((size_t)b * Hkv + g) * capacity + S + r) * hd;
-    ck[kdst + i] = from_f32<TW>(x1 * c - x2 * s);
-    ck[kdst + i + half] = from_f32<TW>(x2 * c + x1 * s);
+    ck[kdst + i] = from_f32<TW>(x1 * cs.x - x2 * cs.y);
+    ck[kdst + i + half] = from_f32<TW>(x2 * cs.x + x1 * cs.y);
   }
   for (int e = tid; e < hd * n1; e += ROPE_THREADS) {  // values: consecutive threads, consecutive slots
     const int dd = e / n1, r = e - dd * n1;
@@ -145,6 +149,14 @@ __global__ void cast_bf16_f16_kernel(const bf16x8 *__restrict__ in, f16x8 *__res
 }  // namespace
 
 namespace acespec {
+
+hipError_t launch_rope_table(const int32_t *pos, const double *inv_freq, float2 *rot, int rows,
+                             int half, hipStream_t s) {
+  const int n = rows * half;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, s, pos, inv_freq,
+                     rot, rows, half);
+  return hipGetLastError();
+}
 
 hipError_t launch_cast_bf16_f16(const bf16 *in, f16 *out, size_t n, hipStream_t s) {
   const size_t n8 = n / 8;  // n is a multiple of 64 (rows x d_model)
@@ -171,12 +183,11 @@ hipError_t launch_rmsnorm(const TIN *x, const TW *gain, typename ActOf<TW>::type
 template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
-                          int Hkv, int hd, int capacity, const double *inv_freq, hipStream_t s) {
+                          int Hkv, int hd, int capacity, const float2 *rot, hipStream_t s) {
   if (n1 > ROPE_MAX_ROWS || hd > 2 * ROPE_MAX_HALF || H % Hkv) return hipErrorInvalidValue;
   hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(Hkv, B),
                      dim3(ROPE_THREADS),
-                     0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity,
-                     inv_freq);
+                     0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity, rot);
   return hipGetLastError();
 }
 
@@ -191,10 +202,10 @@ template hipError_t launch_rmsnorm<bf16, float>(const float *, const bf16 *, f16
 template hipError_t launch_rmsnorm<bf16, bf16>(const bf16 *, const bf16 *, f16 *, int, int,
                                                float, hipStream_t);
 template hipError_t launch_rope_kv<float>(const float *, float *, const TreeMeta &, float *,
-                                          float *, int, int, int, int, int, int, const double *,
+                                          float *, int, int, int, int, int, int, const float2 *,
                                           hipStream_t);
 template hipError_t launch_rope_kv<bf16>(const float *, f16 *, const TreeMeta &, bf16 *, bf16 *,
-                                         int, int, int, int, int, int, const double *,
+                                         int, int, int, int, int, int, const float2 *,
                                          hipStream_t);
 
 }  // namespace acespec

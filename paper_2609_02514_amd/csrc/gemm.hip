@@ -66,7 +66,7 @@ template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
-    int full, int tsplit) {
+    int full, int tsplit, acespec::RopeOut<TB> ro) {
   constexpr int NW = WMN * WNN;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
   constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
@@ -220,6 +220,78 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   }
   // No LDS DMA may still be writing when the workgroup's LDS is released.
   wait_vmcnt<0>();
+
+  if constexpr (EPI == acespec::EPI_QKV_ROPE) {
+    // QKV projection (never sliced along K here): the fp32 tile goes through LDS in
+    // 64-row parts so that each head's rotation pairs (i, i + hd/2) and each value
+    // column's run of consecutive tree slots can be read across waves.
+    constexpr int CR = 64, SP = TBN + 4;  // rows per part, row pitch in floats
+    static_assert(CR * SP * 4 <= NST * STAGE_BYTES, "a part of the tile fits the ring");
+    float *st = (float *)smem;
+    const int hd = ro.hd, half = hd >> 1, nheads = ro.H + 2 * ro.Hkv;
+    for (int c0 = 0; c0 < TBM; c0 += CR) {
+      __syncthreads();  // every wave is past the ring / the previous part
+#pragma unroll
+      for (int ii = 0; ii < WTM; ++ii)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int lrow = wm * WTM * 16 + ii * 16 + lk * 4 + e - c0;
+          if (lrow < 0 || lrow >= CR) continue;
+#pragma unroll
+          for (int j = 0; j < WTN; ++j) st[lrow * SP + wn * WTN * 16 + j * 16 + lr] = acc[ii][j][e];
+        }
+      __syncthreads();
+      for (int hb = 0; hb < TBN / hd; ++hb) {
+        const int gh = tn * (TBN / hd) + hb;  // head of the projection: q, k, then v heads
+        if (gh >= nheads) break;
+        const float *sb = st + hb * hd;
+        if (gh < ro.H + ro.Hkv) {  // query or key head: rotate-half, 4 frequencies a thread
+          const int q4 = half >> 2;
+          for (int it = tid; it < CR * q4; it += NW * 64) {
+            const int r = it / q4, i = (it - r * q4) * 4, row = m0 + c0 + r;
+            if (row >= M) continue;
+            const float4 a1 = *(const float4 *)(sb + r * SP + i);
+            const float4 a2 = *(const float4 *)(sb + r * SP + i + half);
+            const float4 c01 = *(const float4 *)(ro.rot + (size_t)row * half + i);
+            const float4 c23 = *(const float4 *)(ro.rot + (size_t)row * half + i + 2);
+            const float x1[4] = {a1.x, a1.y, a1.z, a1.w}, x2[4] = {a2.x, a2.y, a2.z, a2.w};
+            const float cc[4] = {c01.x, c01.z, c23.x, c23.z}, sn[4] = {c01.y, c01.w, c23.y, c23.w};
+            float y1[4], y2[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              y1[e] = x1[e] * cc[e] - x2[e] * sn[e];
+              y2[e] = x2[e] * cc[e] + x1[e] * sn[e];
+            }
+            if (gh < ro.H) {
+              typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+              f16 *qo = ro.q + (size_t)row * ro.H * hd + (size_t)gh * hd;
+              *(h4 *)(qo + i) = h4{(f16)y1[0], (f16)y1[1], (f16)y1[2], (f16)y1[3]};
+              *(h4 *)(qo + i + half) = h4{(f16)y2[0], (f16)y2[1], (f16)y2[2], (f16)y2[3]};
+            } else {
+              typedef TB t4 __attribute__((ext_vector_type(4)));
+              const int b = row / ro.n1, rr = row - b * ro.n1;
+              TB *kd = ro.ck + (((size_t)b * ro.Hkv + (gh - ro.H)) * ro.capacity +
+                                ro.sess_S[b] + rr) * hd;
+              *(t4 *)(kd + i) = t4{from_f32<TB>(y1[0]), from_f32<TB>(y1[1]),
+                                   from_f32<TB>(y1[2]), from_f32<TB>(y1[3])};
+              *(t4 *)(kd + i + half) = t4{from_f32<TB>(y2[0]), from_f32<TB>(y2[1]),
+                                          from_f32<TB>(y2[2]), from_f32<TB>(y2[3])};
+            }
+          }
+        } else {  // value head: head-dim-major cache, consecutive rows -> consecutive slots
+          const int g = gh - ro.H - ro.Hkv;
+          for (int it = tid; it < CR * hd; it += NW * 64) {
+            const int dd = it / CR, r = it - dd * CR, row = m0 + c0 + r;
+            if (row >= M) continue;
+            const int b = row / ro.n1, rr = row - b * ro.n1;
+            ro.cv[(((size_t)b * ro.Hkv + g) * hd + dd) * ro.capacity + ro.sess_S[b] + rr] =
+                from_f32<TB>(sb[r * SP + dd]);
+          }
+        }
+      }
+    }
+    return;
+  }
 
   // Epilogue.  acc[i][j][e] is C[row = m0 + wm*WTM*16 + i*16 + lk*4 + e][col = .. + lr].
   if (ns > 1) {  // k-slice of a split tile: raw sums at [slice][tile row][W-tile row]
@@ -504,7 +576,8 @@ SplitPlan plan_split(int M, int N, int K, int kss, int tbm, int tbn, int tiles, 
 
 template <int EPI, int V, typename TB>
 void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int K, f16 *out,
-                    float *outf, float *part, int mt, int nt, SplitPlan sp) {
+                    float *outf, float *part, int mt, int nt, SplitPlan sp,
+                    const acespec::RopeOut<TB> &ro) {
   constexpr GemmVariant v = kVariants[V];
   constexpr int TBM = v.wmn * v.wtm * 16, TBN = v.wnn * v.wtn * 16;
   const int tiles = mt * nt;
@@ -512,7 +585,7 @@ void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int 
   hipLaunchKernelGGL(
         (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>),
         dim3(units), dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
-        sp.full, sp.tsplit);
+        sp.full, sp.tsplit, ro);
   if (sp.tsplit > 1) {
     const int nsplit_tiles = tiles - sp.full;
     const long long threads =
@@ -525,9 +598,10 @@ void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int 
 
 template <int EPI, typename TB>
 void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N, int K,
-                f16 *out, float *outf, float *part, int mt, int nt, SplitPlan sp) {
+                f16 *out, float *outf, float *part, int mt, int nt, SplitPlan sp,
+                const acespec::RopeOut<TB> &ro = acespec::RopeOut<TB>{}) {
   switch (var) {
-#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp); break;
+#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro); break;
     CASE(0) CASE(1) CASE(2) CASE(3)
 #undef CASE
     default: break;
@@ -610,7 +684,7 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
     hipLaunchKernelGGL(                                                                     \
         (gemm_f16w_kernel<EPI_RESID, bf16, g.wmn, g.wnn, g.wtm, g.wtn, g.nst, g.occ, g.kss>), \
         dim3(mt * nt * sp.tsplit), dim3(g.wmn * g.wnn * 64), 0, s, A, W, M, N, K, nullptr,   \
-        x, aux.part, mt, nt, 0, sp.tsplit);                                                 \
+        x, aux.part, mt, nt, 0, sp.tsplit, RopeOut<bf16>{});                                \
     launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
     break;                                                                                  \
   }
@@ -664,6 +738,39 @@ hipError_t launch_gemm_resid_norm<float, float>(const float *A, const float *W, 
   hipError_t e = launch_gemm<float, float>(EPI_RESID, A, W, M, N, K, nullptr, x, aux, s);
   if (e != hipSuccess) return e;
   return launch_rmsnorm<float, float>(x, gain, out, M, N, eps, s);
+}
+
+template <>
+hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
+                                      float *qkv, const RopeOut<bf16> &ro, const TreeMeta &meta,
+                                      int B, const GemmAux &aux, hipStream_t s) {
+  const int var = pick_variant(EPI_F32, M, N, K);
+  const GemmVariant v = kVariants[var];
+  const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
+  const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
+  const SplitPlan sp =
+      plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  if (sp.tsplit == 1 && tbn % ro.hd == 0 && N == (ro.H + 2 * ro.Hkv) * ro.hd) {
+    launch_epi<EPI_QKV_ROPE, bf16>(var, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
+                                   sp, ro);
+    return hipGetLastError();
+  }
+  hipError_t e = launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, qkv,
+                                           aux.part, aux.part_cap, aux.cus, s);
+  if (e != hipSuccess) return e;
+  return launch_rope_kv<bf16>(qkv, ro.q, meta, ro.ck, ro.cv, B, ro.n1, ro.H, ro.Hkv, ro.hd,
+                              ro.capacity, ro.rot, s);
+}
+
+template <>
+hipError_t launch_qkv_rope<float, float>(const float *A, const float *W, int M, int N, int K,
+                                         float *qkv, const RopeOut<float> &ro,
+                                         const TreeMeta &meta, int B, const GemmAux &aux,
+                                         hipStream_t s) {
+  hipError_t e = launch_gemm<float, float>(EPI_F32, A, W, M, N, K, nullptr, qkv, aux, s);
+  if (e != hipSuccess) return e;
+  return launch_rope_kv<float>(qkv, ro.q, meta, ro.ck, ro.cv, B, ro.n1, ro.H, ro.Hkv, ro.hd,
+                               ro.capacity, ro.rot, s);
 }
 
 }  // namespace acespec
