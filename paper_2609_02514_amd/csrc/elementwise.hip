@@ -4,9 +4,11 @@
 // activation type.  The residual stream x stays fp32 between layers.
 // RoPE (rotate-half): the pair (i, i + hd/2) of every query and key head is rotated by
 // pos * base^(-2i/hd); the angle and its sine/cosine are evaluated in double so that
-// large positions (16k-token prefixes) keep full fp32 accuracy.  The QKV projection
-// arrives in fp32 and is rounded once: q to the activation type, k and v to the cache
-// dtype.  Tree row r of session b sits at position prefix_len + depth(r) and its
+// large positions (16k-token prefixes) keep full fp32 accuracy, once per step into a
+// (cos, sin) table of fp32 pairs per tree row.  The rotation itself normally runs in the
+// QKV projection's epilogue; the kernel here serves the fp32 model and products sliced
+// along K.  The projection is rounded once: q to the activation type, k and v to the
+// cache dtype.  Tree row r of session b sits at position prefix_len + depth(r) and its
 // key/value go to slot prefix_len + r.
 #include "common.h"
 
