@@ -221,7 +221,7 @@ def main():
 
     import torch
     import synth
-    from paper_2609_02514_amd.acespec import (Verifier, acespec_timing_enable,
+    from paper_2609_02514_amd.acespec import (Verifier, acespec_timing_enable, acespec_timing_only,
                                               acespec_timing_read)
 
     torch.cuda.set_device(0)
@@ -248,7 +248,39 @@ def main():
         step()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
+    work = kernel_work(w, B, n1, P, S_tot)
+
+    def breakdown(per_kernel, nsteps):
+        kernels = {}
+        for name, (ms, cnt) in per_kernel.items():
+            avg = ms / max(cnt, 1)
+            ent = {"ms_per_step": round(ms / nsteps, 4), "avg_launch_ms": round(avg, 5),
+                   "launches_per_step": cnt // nsteps}
+            if name in work:
+                fl, by = work[name]
+                if fl and name.startswith("gemm"):
+                    ent["tflops"] = round(fl / (avg / 1e3) / 1e12, 1)
+                    ent["mfma_frac"] = round(ent["tflops"] / PEAK_MFMA_TFLOPS, 4)
+                if by:
+                    ent["gbs"] = round(by / (avg / 1e3) / 1e9, 1)
+                    ent["hbm_frac"] = round(ent["gbs"] / PEAK_HBM_GBS, 4)
+            kernels[name] = ent
+        return kernels
+
+    # Per-kernel breakdown: the same steps with HIP events around every kernel (each
+    # recorded pair costs stream time, so this pass is kept out of the timed region).
+    acespec_timing_only(v.ctx, None)
     acespec_timing_enable(v.ctx, True)
+    acespec_timing_read(v.ctx)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kernels = breakdown(acespec_timing_read(v.ctx), args.steps)
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+
+    # Timed region: events only around the dominant kernel kind (its launches give the
+    # roofline's average duration, measured on the launch stream).
+    acespec_timing_only(v.ctx, dom)
     acespec_timing_read(v.ctx)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -260,35 +292,19 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     ms_total = e0.elapsed_time(e1)
-    per_kernel = acespec_timing_read(v.ctx)
+    dk = breakdown(acespec_timing_read(v.ctx), args.steps)[dom]
     acespec_timing_enable(v.ctx, False)
+    acespec_timing_only(v.ctx, None)
     ms_step = ms_total / args.steps
     tokens = B * (n1 - 1)
     value = tokens / (ms_step / 1e3)
     log(f"{args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f}), "
         f"{value:.0f} tok/s; status {outs['status'].tolist()[:4]}...")
 
-    work = kernel_work(w, B, n1, P, S_tot)
-    kernels = {}
-    for name, (ms, cnt) in per_kernel.items():
-        avg = ms / max(cnt, 1)
-        ent = {"ms_per_step": round(ms / args.steps, 4), "avg_launch_ms": round(avg, 5),
-               "launches_per_step": cnt // args.steps}
-        if name in work:
-            fl, by = work[name]
-            if fl and name.startswith("gemm"):
-                ent["tflops"] = round(fl / (avg / 1e3) / 1e12, 1)
-                ent["mfma_frac"] = round(ent["tflops"] / PEAK_MFMA_TFLOPS, 4)
-            if by:
-                ent["gbs"] = round(by / (avg / 1e3) / 1e9, 1)
-                ent["hbm_frac"] = round(ent["gbs"] / PEAK_HBM_GBS, 4)
-        kernels[name] = ent
     traffic = load_traffic(w.name)
     for name, ent in kernels.items():
         if name in traffic:
             ent["hbm_traffic_bytes_per_launch"] = traffic[name]
-    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
-    dk = kernels[dom]
     if dom.startswith("gemm"):
         roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dk["mfma_frac"],
@@ -345,6 +361,8 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,
+        "kernels_timing": "separate pass of the same steps with HIP events around every kernel "
+                          "(the timed region records events around the roofline kernel only)",
         "commit_kv": commit,
     }
     print(json.dumps(line), flush=True)

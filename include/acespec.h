@@ -210,6 +210,11 @@ const char *acespec_last_error(void);
 int acespec_timing_enable(acespec_ctx *ctx, int enable);
 int acespec_timing_read(acespec_ctx *ctx, const char **names, double *total_ms,
                         int *launches, int max);
+/* Restricts the timing events to the kernels of one kind (a name acespec_timing_read
+ * reports, e.g. "gemm_gate_up"); NULL restores every kind.  Each timed launch adds two
+ * event records to the stream, so timing one kind keeps the cost to the measured step
+ * small.  Unknown names return ACESPEC_EINVAL and leave the selection unchanged. */
+int acespec_timing_only(acespec_ctx *ctx, const char *kind);
 
 #ifdef __cplusplus
 }

@@ -19,7 +19,8 @@ ACESPEC_F32, ACESPEC_BF16 = 0, 1
 
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",
             "acespec_verify_tree_scalar_q", "acespec_verify_tail", "acespec_commit_kv",
-            "acespec_last_error", "acespec_timing_enable", "acespec_timing_read"]
+            "acespec_last_error", "acespec_timing_enable", "acespec_timing_read",
+            "acespec_timing_only"]
 
 
 class ModelDesc(C.Structure):
@@ -94,6 +95,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.acespec_timing_read.argtypes = [C.c_void_p, C.POINTER(C.c_char_p),
                                         C.POINTER(C.c_double), C.POINTER(C.c_int), C.c_int]
     lib.acespec_timing_read.restype = C.c_int
+    lib.acespec_timing_only.argtypes = [C.c_void_p, C.c_char_p]
+    lib.acespec_timing_only.restype = C.c_int
     _lib = lib
     return lib
 
@@ -162,6 +165,10 @@ def acespec_commit_kv(ctx, kv: KVCache, path: int, path_len: int, status: Option
 
 def acespec_timing_enable(ctx, enable: bool) -> None:
     _check(load().acespec_timing_enable(ctx, 1 if enable else 0))
+
+
+def acespec_timing_only(ctx, kind: Optional[str]) -> None:
+    _check(load().acespec_timing_only(ctx, kind.encode() if kind else None))
 
 
 def acespec_timing_read(ctx) -> Dict[str, tuple]:

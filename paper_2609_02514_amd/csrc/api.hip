@@ -63,6 +63,7 @@ struct acespec_ctx {
   TreeMeta meta{};
   // timing
   bool timing = false;
+  uint32_t timing_mask = ~0u;  // kinds timed while timing is on
   struct Rec { int kind; hipEvent_t e0, e1; };
   std::vector<hipEvent_t> free_events;
   std::vector<Rec> pending;
@@ -87,7 +88,8 @@ hipEvent_t get_event(acespec_ctx *c) {
 template <typename F>
 int run(acespec_ctx *c, int kind, hipStream_t s, F &&launch) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (c->timing) {
+  const bool timed = c->timing && ((c->timing_mask >> kind) & 1u);
+  if (timed) {
     e0 = get_event(c);
     e1 = get_event(c);
     if (!e0 || !e1) return fail(ACESPEC_EHIP, "hipEventCreate failed");
@@ -96,7 +98,7 @@ int run(acespec_ctx *c, int kind, hipStream_t s, F &&launch) {
   hipError_t err = launch();
   if (err != hipSuccess)
     return fail(ACESPEC_EHIP, "%s launch failed: %s", kKindNames[kind], hipGetErrorString(err));
-  if (c->timing) {
+  if (timed) {
     if (hipEventRecord(e1, s) != hipSuccess) return fail(ACESPEC_EHIP, "hipEventRecord failed");
     c->pending.push_back({kind, e0, e1});
   }
@@ -507,6 +509,20 @@ int acespec_timing_enable(acespec_ctx *ctx, int enable) {
   if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
   ctx->timing = enable != 0;
   return ACESPEC_OK;
+}
+
+int acespec_timing_only(acespec_ctx *ctx, const char *kind) {
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  if (!kind) {
+    ctx->timing_mask = ~0u;
+    return ACESPEC_OK;
+  }
+  for (int k = 0; k < K_COUNT; ++k)
+    if (std::strcmp(kind, kKindNames[k]) == 0) {
+      ctx->timing_mask = 1u << k;
+      return ACESPEC_OK;
+    }
+  return fail(ACESPEC_EINVAL, "unknown kernel kind '%s'", kind);
 }
 
 int acespec_timing_read(acespec_ctx *ctx, const char **names, double *total_ms, int *launches,
