@@ -60,6 +60,7 @@ struct acespec_ctx {
   int cus = 256;
   double *inv_freq = nullptr;
   float2 *rot = nullptr;      // RoPE (cos, sin) per tree row and frequency, per step
+  float *tile_max = nullptr;  // LM-head row maxima per column tile
   TreeMeta meta{};
   // timing
   bool timing = false;
@@ -177,12 +178,15 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
     RUN(K_GEMM_DOWN, (launch_gemm_resid_norm<T, A>(x_h, (const T *)lw.w_down, R, D, F, ctx->x,
                                                    next_norm, x_a, d.rms_eps, aux, stream)));
   }
-  RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, x_a, (const T *)w->lm_head, R, V, D, nullptr,
-                                    logits, aux, stream)));
-  VocabArgs va;
+  int ntile = 0;
+  RUN(K_GEMM_LM, (launch_lm_head<T, A>(x_a, (const T *)w->lm_head, R, V, D, logits,
+                                       ctx->tile_max, &ntile, aux, stream)));
+  VocabArgs va{};
   va.logits = logits;
   va.q = draft_q;
   va.q_scalar = q_scalar;
+  va.tile_max = ntile ? ctx->tile_max : nullptr;
+  va.ntile = ntile;
   va.u = uniforms;
   va.tok = meta.tok;
   va.par = meta.par;
@@ -229,7 +233,7 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
     RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)hidden, (const T *)lm_head, R, V, D,
                                       nullptr, logits, aux, stream)));
   }
-  VocabArgs va;
+  VocabArgs va{};
   va.logits = logits;
   va.q = draft_q;
   va.q_scalar = nullptr;
@@ -303,7 +307,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
-  void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr;
+  void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr, *p_tmax = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
@@ -314,6 +318,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       {layers ? R * d.n_heads * d.head_dim * c->esz : 0, &c->q},
       {layers ? R * d.d_ff * c->esz : 0, &c->h},
       {R * (size_t)d.vocab * 4, &p_logits},
+      {R * (size_t)((d.vocab + 127) / 128) * 4, &p_tmax},
       {(size_t)c->part_cap * 4, &p_po},
       {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
       {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
@@ -348,6 +353,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_ml = (float *)p_pml;
   c->inv_freq = (double *)p_if;
   c->rot = (float2 *)p_rot;
+  c->tile_max = (float *)p_tmax;
   c->meta.tok = (int32_t *)p_tok;
   c->meta.par = (int32_t *)p_par;
   c->meta.pos = (int32_t *)p_pos;

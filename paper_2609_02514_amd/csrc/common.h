@@ -163,7 +163,8 @@ hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           int Hkv, int hd, int capacity, const float2 *rot, hipStream_t s);
 
 
-enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3, EPI_QKV_ROPE = 4 };
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3, EPI_QKV_ROPE = 4,
+               EPI_F32_MAX = 5 };
 
 // C[M, N] = A[M, K] . W[N, K]^T with the epilogue:
 //  EPI_STORE : out (activation type) [M, N]
@@ -172,6 +173,8 @@ enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_F32 = 3, EPI_QK
 //  EPI_F32   : outf (fp32) [M, N] = C
 //  EPI_QKV_ROPE: C is the QKV projection; RoPE, rounding and the cache write of the tree
 //              rows happen in the epilogue (see launch_qkv_rope)
+//  EPI_F32_MAX: as EPI_F32, and the maximum of every row over each column tile
+//              (see launch_lm_head)
 // A is in the activation type.  aux.part: fp32 workspace for split-K partials
 // (aux.part_cap floats), aux.cus: compute units of the device.
 struct GemmAux {
@@ -195,6 +198,14 @@ template <typename TW, typename TA>
 hipError_t launch_qkv_rope(const TA *A, const TW *W, int M, int N, int K, float *qkv,
                            const RopeOut<TW> &ro, const TreeMeta &meta, int B,
                            const GemmAux &aux, hipStream_t s);
+
+// The LM head: fp32 logits [M, N] = A . W^T.  When the product is not sliced along K the
+// epilogue also writes tile_max[row * ntile + t], the maximum of row `row` over column
+// tile t, and *ntile is set (else *ntile = 0): the vocabulary kernel then takes a row's
+// maximum from ntile values instead of a pass over the row.
+template <typename TW, typename TA>
+hipError_t launch_lm_head(const TA *A, const TW *W, int M, int N, int K, float *logits,
+                          float *tile_max, int *ntile, const GemmAux &aux, hipStream_t s);
 
 template <typename TW, typename TA>
 hipError_t launch_gemm(int epi, const TA *A, const TW *W, int M, int N, int K,
@@ -233,6 +244,8 @@ struct VocabArgs {
   const float *logits;      // [rows, V]
   const float *q;           // [rows, V] dense draft distributions (NULL in scalar mode)
   const float *q_scalar;    // [rows] q-hat of each row's own token, or NULL (dense mode)
+  const float *tile_max;    // [rows, ntile] row maxima over column tiles, or NULL
+  int ntile;
   const float *u;           // [rows, 3]
   const int32_t *tok;       // [rows] token of each row (children look theirs up here)
   const int32_t *par;       // [rows] parent row within the session, -1 for the root

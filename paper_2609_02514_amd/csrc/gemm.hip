@@ -338,6 +338,32 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
       }
     }
   }
+  if constexpr (EPI == acespec::EPI_F32_MAX) {
+    // row maxima over this tile's columns (padding columns repeat the last real one):
+    // over the wave's blocks in registers, its 16 column lanes by shuffles, then the
+    // WNN waves of a row through LDS; `part` holds [M][nt]
+    __syncthreads();  // every wave is past the ring
+    float *red = (float *)smem;  // [WNN][TBM]
+#pragma unroll
+    for (int ii = 0; ii < WTM; ++ii)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float m = acc[ii][0][e];
+#pragma unroll
+        for (int j = 1; j < WTN; ++j) m = fmaxf(m, acc[ii][j][e]);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+        if (lr == 0) red[wn * TBM + wm * WTM * 16 + ii * 16 + lk * 4 + e] = m;
+      }
+    __syncthreads();
+    for (int r = tid; r < TBM; r += NW * 64) {
+      if (m0 + r >= M) break;
+      float m = red[r];
+#pragma unroll
+      for (int q = 1; q < WNN; ++q) m = fmaxf(m, red[q * TBM + r]);
+      part[(size_t)(m0 + r) * nt + tn] = m;
+    }
+  }
 }
 
 // Sums the k-slices of the split tiles in a fixed order (deterministic) and applies the
@@ -516,6 +542,7 @@ using acespec::EPI_STORE;
 using acespec::EPI_RESID;
 using acespec::EPI_SWIGLU;
 using acespec::EPI_F32;
+using acespec::EPI_F32_MAX;
 
 // Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU,
 // k per stage}.  Measured on MI355X against the verify-step shapes.  Tried and slower on
@@ -771,6 +798,33 @@ hipError_t launch_qkv_rope<float, float>(const float *A, const float *W, int M, 
   if (e != hipSuccess) return e;
   return launch_rope_kv<float>(qkv, ro.q, meta, ro.ck, ro.cv, B, ro.n1, ro.H, ro.Hkv, ro.hd,
                                ro.capacity, ro.rot, s);
+}
+
+template <>
+hipError_t launch_lm_head<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
+                                     float *logits, float *tile_max, int *ntile,
+                                     const GemmAux &aux, hipStream_t s) {
+  *ntile = 0;
+  const int var = pick_variant(EPI_F32, M, N, K);
+  const GemmVariant v = kVariants[var];
+  const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
+  const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
+  const SplitPlan sp =
+      plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  if (sp.tsplit != 1 || tile_max == nullptr)
+    return launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, logits, aux.part,
+                                     aux.part_cap, aux.cus, s);
+  launch_epi<EPI_F32_MAX, bf16>(var, s, A, W, M, N, K, nullptr, logits, tile_max, mt, nt, sp);
+  *ntile = nt;
+  return hipGetLastError();
+}
+
+template <>
+hipError_t launch_lm_head<float, float>(const float *A, const float *W, int M, int N, int K,
+                                        float *logits, float *, int *ntile, const GemmAux &aux,
+                                        hipStream_t s) {
+  *ntile = 0;
+  return launch_gemm<float, float>(EPI_F32, A, W, M, N, K, nullptr, logits, aux, s);
 }
 
 }  // namespace acespec

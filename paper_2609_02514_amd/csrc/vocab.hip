@@ -298,12 +298,17 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
 
   // ---- pass 0: row max -----------------------------------------------------------
   float mx = -INFINITY;
-  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
-    float4 vv[VU];
-    load_step(z, V, i0, vv);
+  if (a.tile_max) {  // the LM head's epilogue left the row's maximum per column tile
+    const float *tm = a.tile_max + (size_t)row * a.ntile;
+    for (int t = tid; t < a.ntile; t += VT) mx = fmaxf(mx, tm[t]);
+  } else {
+    for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
+      float4 vv[VU];
+      load_step(z, V, i0, vv);
 #pragma unroll
-    for (int u = 0; u < VU; ++u)
-      mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
+      for (int u = 0; u < VU; ++u)
+        mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
+    }
   }
   Sel sel;
   sel.M = block_max(mx, sm);

@@ -268,3 +268,36 @@ def test_run_to_run_bitwise_determinism():
     for k in res[0]:
         assert torch.equal(res[0][k], res[1][k]), k
     v.close()
+
+
+def test_timing_selection():
+    """acespec_timing_only restricts the recorded kernels to one kind; unknown kinds are
+    rejected synchronously; NULL restores every kind."""
+    from paper_2609_02514_amd import acespec as A
+    w = small_bf16(B=2)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda")
+    v = A.Verifier.for_workload(w)
+    B, n1 = batch.tokens.shape
+    ws = v.weights_struct(W)
+    outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)
+
+    def step():
+        v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
+                      batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
+
+    A.acespec_timing_enable(v.ctx, True)
+    A.acespec_timing_only(v.ctx, "gemm_gate_up")
+    A.acespec_timing_read(v.ctx)
+    step()
+    got = A.acespec_timing_read(v.ctx)
+    assert list(got) == ["gemm_gate_up"] and got["gemm_gate_up"][1] == w.L
+    with pytest.raises(A.AcespecError) as e:
+        A.acespec_timing_only(v.ctx, "no_such_kernel")
+    assert e.value.code == -1
+    A.acespec_timing_only(v.ctx, None)
+    step()
+    got = A.acespec_timing_read(v.ctx)
+    assert {"gemm_gate_up", "tree_attention", "vocab_verify", "path_walk"} <= set(got)
+    A.acespec_timing_enable(v.ctx, False)
+    v.close()
