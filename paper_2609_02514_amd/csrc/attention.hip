@@ -309,30 +309,42 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   }
 }
 
-// Merge of the split partials: one block per (kv head, session), one thread per value.
-// part_ml holds (max in base-2 exponent units, sum) per (item, query row).
+// Merge of the split partials.  grid: (ceil(QR * HD / 4 / 256), kv heads, sessions); one
+// thread per 4 head dims of one query row.  part_ml holds (max in base-2 exponent units,
+// sum) per (item, query row).
 template <typename T>
-__global__ void attn_combine_kernel(const float *__restrict__ part_o,
-                                    const float *__restrict__ part_ml, T *__restrict__ out,
-                                    int n1, int H, int Hkv, int HD, int nsplit) {
-  const int g = blockIdx.x, b = blockIdx.y;
-  const int G = H / Hkv, QR = G * n1;
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float *__restrict__ part_o,
+                                                           const float *__restrict__ part_ml,
+                                                           T *__restrict__ out, int n1, int H,
+                                                           int Hkv, int HD, int nsplit) {
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int G = H / Hkv, QR = G * n1, hd4 = HD >> 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= QR * hd4) return;
+  const int qi = idx / hd4, d = (idx - qi * hd4) * 4;
   const size_t item0 = ((size_t)b * Hkv + g) * nsplit;
-  for (int idx = threadIdx.x; idx < QR * HD; idx += blockDim.x) {
-    const int qi = idx / HD, d = idx - qi * HD;
-    float M = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, part_ml[((item0 + s) * QR + qi) * 2]);
-    float num = 0.f, den = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const float m = part_ml[((item0 + s) * QR + qi) * 2];
-      if (m == -INFINITY) continue;
-      const float w = exp2f(m - M);
-      den += w * part_ml[((item0 + s) * QR + qi) * 2 + 1];
-      num += w * part_o[((item0 + s) * QR + qi) * HD + d];
-    }
-    const int r = qi / G, h = g * G + (qi - r * G);
-    out[((size_t)b * n1 + r) * (H * HD) + h * HD + d] = from_f32<T>(den > 0.f ? num / den : 0.f);
+  float M = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) M = fmaxf(M, part_ml[((item0 + s) * QR + qi) * 2]);
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+  for (int s = 0; s < nsplit; ++s) {
+    const float m = part_ml[((item0 + s) * QR + qi) * 2];
+    if (m == -INFINITY) continue;
+    const float w = exp2f(m - M);
+    den += w * part_ml[((item0 + s) * QR + qi) * 2 + 1];
+    const float4 v = *(const float4 *)(part_o + ((item0 + s) * QR + qi) * HD + d);
+    num.x += w * v.x;
+    num.y += w * v.y;
+    num.z += w * v.z;
+    num.w += w * v.w;
   }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const int r = qi / G, h = g * G + (qi - r * G);
+  T *o = out + ((size_t)b * n1 + r) * (H * HD) + h * HD + d;
+  o[0] = from_f32<T>(num.x * inv);
+  o[1] = from_f32<T>(num.y * inv);
+  o[2] = from_f32<T>(num.z * inv);
+  o[3] = from_f32<T>(num.w * inv);
 }
 
 // fp32 path: one wave per (tree row, query head); lane i owns dims i and i + 64.
@@ -420,8 +432,9 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
 #undef GO
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nsplit == 1) return e;
-  hipLaunchKernelGGL(attn_combine_kernel<f16>, dim3(Hkv, B), dim3(256), 0, s, part_o, part_ml,
-                     out, n1, H, Hkv, hd, nsplit);
+  const int cblocks = (QR * (hd / 4) + 255) / 256;
+  hipLaunchKernelGGL(attn_combine_kernel<f16>, dim3(cblocks, Hkv, B), dim3(256), 0, s, part_o,
+                     part_ml, out, n1, H, Hkv, hd, nsplit);
   return hipGetLastError();
 }
 
