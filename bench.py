@@ -183,6 +183,35 @@ def cpu_baseline(w, W, batch, n_sessions):
                        f"layers, verify stage of every row, walk; {t:.1f} s")}
 
 
+def cpu_baseline_tail(w, W, batch, n_chains):
+    """The oracle as it stands on n_chains whole chains of the LM-head tail: logits of every
+    row in float64, the verify stage of every row and the chain walk."""
+    import numpy as np
+    from oracle import model as om
+    from oracle import verify as ov
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    rows = list(range(min(n_chains * w.chain_len, w.rows)))
+    Wh = type(W)(None, [], None, W.lm_head.cpu())
+    hid = batch.hidden[rows].cpu()
+    q = batch.q[rows].cpu().numpy().astype(np.float64)
+    u = batch.u[rows].cpu().numpy().astype(np.float64)
+    d = batch.draft_tokens[rows].cpu().numpy()
+    t0 = time.perf_counter()
+    z = om.lm_head_tail(Wh, hid)
+    res = ov.verify_tail(z, q, d, u, w.T, w.top_p, w.top_k, w.chain_len)
+    ov.walk_tail(res["accept"], res["resample"], w.chain_len)
+    t = time.perf_counter() - t0
+    return {"value": len(rows) / t, "unit": "verified tree tokens/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"{len(rows) // w.chain_len} of {w.rows // w.chain_len} chains of {w.name} "
+                       f"({len(rows)} rows): float64 LM head, verify stage of every row, chain "
+                       f"walk; {t:.1f} s")}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,22 +255,33 @@ def main():
 
     torch.cuda.set_device(0)
     w = synth.get(args.workload)
-    if w.tree == "tail":
-        raise SystemExit("bench.py times the full tree-verify step; pick a tree workload")
+    tail = w.tree == "tail"
     log(f"generating {w.name} on the GPU")
     W = synth.make_weights(w, "cuda")
     batch = synth.make_batch(w, "cuda")
-    B, n1 = batch.tokens.shape
-    parents = synth.tree_parents(w)
-    P = sum(1 for c in synth.children_lists(parents) if c) * B
-    S_tot = int(batch.prefix_len.sum().item()) + B * n1
     v = Verifier.for_workload(w)
-    ws = v.weights_struct(W)
-    outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)
+    if tail:
+        # LM head + vocabulary verify over given hidden states: every row is the parent of
+        # one drafted token (acespec_verify_tail); B chains of chain_len rows.
+        R = w.rows
+        B, n1 = R // w.chain_len, w.chain_len
+        P, S_tot = R, 0
+        outs = v.alloc_outputs(R, B, n1, w.top_k, w.V, "cuda", False)
 
-    def step():
-        v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
-                      batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
+        def step():
+            v.verify_tail(W.lm_head, None, batch.hidden, batch.draft_tokens, batch.q, batch.u,
+                          w.chain_len, w.T, w.top_p, w.top_k, outs)
+    else:
+        B, n1 = batch.tokens.shape
+        parents = synth.tree_parents(w)
+        P = sum(1 for c in synth.children_lists(parents) if c) * B
+        S_tot = int(batch.prefix_len.sum().item()) + B * n1
+        ws = v.weights_struct(W)
+        outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)
+
+        def step():
+            v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
+                          batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
 
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
@@ -296,7 +336,7 @@ def main():
     acespec_timing_enable(v.ctx, False)
     acespec_timing_only(v.ctx, None)
     ms_step = ms_total / args.steps
-    tokens = B * (n1 - 1)
+    tokens = B * n1 if tail else B * (n1 - 1)   # drafted tokens verified per step
     value = tokens / (ms_step / 1e3)
     log(f"{args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f}), "
         f"{value:.0f} tok/s; status {outs['status'].tolist()[:4]}...")
@@ -337,7 +377,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host (bounded sample)")
-        cpu = cpu_baseline(w, W, batch, args.cpu_sessions)
+        cpu = (cpu_baseline_tail(w, W, batch, args.cpu_sessions * 32) if tail
+               else cpu_baseline(w, W, batch, args.cpu_sessions))
         log(f"oracle: {cpu['value']:.3f} tok/s on {cpu['cores']} threads")
 
     line = {
@@ -354,10 +395,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16 weights/KV, fp16 activations on f16 MFMA, fp32 accumulate",
         "data": "synthetic (seeded random-init weights, KV prefix, drafted trees, draft q)",
-        "config": {"workload": w.name, "layers": w.L, "d_model": w.d, "heads": w.H,
-                   "kv_heads": w.Hkv, "head_dim": w.hd, "d_ff": w.F, "vocab": w.V,
-                   "sessions": B, "prefix_len": w.S, "drafted_nodes": n1 - 1,
-                   "temperature": w.T, "top_p": w.top_p, "top_k": w.top_k},
+        "config": ({"workload": w.name, "d_model": w.d, "vocab": w.V, "rows": B * n1,
+                    "chain_len": n1, "temperature": w.T, "top_p": w.top_p, "top_k": w.top_k}
+                   if tail else
+                   {"workload": w.name, "layers": w.L, "d_model": w.d, "heads": w.H,
+                    "kv_heads": w.Hkv, "head_dim": w.hd, "d_ff": w.F, "vocab": w.V,
+                    "sessions": B, "prefix_len": w.S, "drafted_nodes": n1 - 1,
+                    "temperature": w.T, "top_p": w.top_p, "top_k": w.top_k}),
         "roofline": roof,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -219,24 +219,25 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   const int D = d.d_model, V = d.vocab;
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
   const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus};
+  const A *h_in = (const A *)hidden;
   if (final_norm) {
     RUN(K_RMSNORM, (launch_rmsnorm<T, T>((const T *)hidden, (const T *)final_norm, (A *)ctx->a,
                                          R, D, d.rms_eps, stream)));
-    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)ctx->a, (const T *)lm_head, R, V, D,
-                                      nullptr, logits, aux, stream)));
+    h_in = (const A *)ctx->a;
   } else if (sizeof(T) == 2) {  // bf16 hidden states: widen to fp16 for the f16 MFMA path
     RUN(K_RMSNORM, launch_cast_bf16_f16((const bf16 *)hidden, (f16 *)ctx->a, (size_t)R * D,
                                         stream));
-    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)ctx->a, (const T *)lm_head, R, V, D,
-                                      nullptr, logits, aux, stream)));
-  } else {
-    RUN(K_GEMM_LM, (launch_gemm<T, A>(EPI_F32, (const A *)hidden, (const T *)lm_head, R, V, D,
-                                      nullptr, logits, aux, stream)));
+    h_in = (const A *)ctx->a;
   }
+  int ntile = 0;
+  RUN(K_GEMM_LM, (launch_lm_head<T, A>(h_in, (const T *)lm_head, R, V, D, logits,
+                                       ctx->tile_max, &ntile, aux, stream)));
   VocabArgs va{};
   va.logits = logits;
   va.q = draft_q;
   va.q_scalar = nullptr;
+  va.tile_max = ntile ? ctx->tile_max : nullptr;
+  va.ntile = ntile;
   va.u = uniforms;
   va.tok = draft;
   va.par = nullptr;

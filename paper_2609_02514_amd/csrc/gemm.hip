@@ -66,7 +66,7 @@ template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
-    int full, int tsplit, acespec::RopeOut<TB> ro) {
+    int full, int tsplit, acespec::RopeOut<TB> ro, float *__restrict__ tmax) {
   constexpr int NW = WMN * WNN;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
   constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
@@ -341,7 +341,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   if constexpr (EPI == acespec::EPI_F32_MAX) {
     // row maxima over this tile's columns (padding columns repeat the last real one):
     // over the wave's blocks in registers, its 16 column lanes by shuffles, then the
-    // WNN waves of a row through LDS; `part` holds [M][nt]
+    // WNN waves of a row through LDS; tmax holds [M][nt]
     __syncthreads();  // every wave is past the ring
     float *red = (float *)smem;  // [WNN][TBM]
 #pragma unroll
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
       float m = red[r];
 #pragma unroll
       for (int q = 1; q < WNN; ++q) m = fmaxf(m, red[q * TBM + r]);
-      part[(size_t)(m0 + r) * nt + tn] = m;
+      tmax[(size_t)(m0 + r) * nt + tn] = m;
     }
   }
 }
@@ -374,7 +374,8 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
                                                          f16 *__restrict__ out,
                                                          float *__restrict__ outf, int M, int N,
                                                          int mt, int full, int nsplit_tiles,
-                                                         int tsplit) {
+                                                         int tsplit, float *__restrict__ tmax,
+                                                         int nt) {
   constexpr int CW = (EPI == acespec::EPI_SWIGLU ? TBN / 2 : TBN) / 4;  // threads per row
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= (long long)nsplit_tiles * TBM * CW) return;
@@ -383,7 +384,7 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
   const int lrow = rem / CW, c4 = (rem - lrow * CW) * 4;
   const int tile = full + t, tn = tile / mt, tm = tile - tn * mt;
   const int row = tm * TBM + lrow;
-  if (row >= M) return;
+  if (EPI != acespec::EPI_F32_MAX && row >= M) return;
   const float *pt = part + (size_t)t * tsplit * (TBM * TBN) + (size_t)lrow * TBN + c4;
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f), g = a;
   for (int sp = 0; sp < tsplit; ++sp) {
@@ -393,6 +394,14 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
       const float4 u = *(const float4 *)(pt + (size_t)sp * (TBM * TBN) + TBN / 2);
       g.x += u.x; g.y += u.y; g.z += u.z; g.w += u.w;
     }
+  }
+  if constexpr (EPI == acespec::EPI_F32_MAX) {
+    // the CW threads of a tile row are CW consecutive lanes of one wave (CW divides 64)
+    float m = fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w));
+#pragma unroll
+    for (int o = 1; o < CW; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+    if (row >= M) return;
+    if (c4 == 0) tmax[(size_t)row * nt + tn] = m;
   }
   const float av[4] = {a.x, a.y, a.z, a.w}, uv[4] = {g.x, g.y, g.z, g.w};
   const int col0 = tn * (EPI == acespec::EPI_SWIGLU ? TBN / 2 : TBN) + c4;
@@ -604,7 +613,7 @@ SplitPlan plan_split(int M, int N, int K, int kss, int tbm, int tbn, int tiles, 
 template <int EPI, int V, typename TB>
 void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int K, f16 *out,
                     float *outf, float *part, int mt, int nt, SplitPlan sp,
-                    const acespec::RopeOut<TB> &ro) {
+                    const acespec::RopeOut<TB> &ro, float *tmax) {
   constexpr GemmVariant v = kVariants[V];
   constexpr int TBM = v.wmn * v.wtm * 16, TBN = v.wnn * v.wtn * 16;
   const int tiles = mt * nt;
@@ -612,23 +621,24 @@ void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int 
   hipLaunchKernelGGL(
         (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>),
         dim3(units), dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
-        sp.full, sp.tsplit, ro);
+        sp.full, sp.tsplit, ro, tmax);
   if (sp.tsplit > 1) {
     const int nsplit_tiles = tiles - sp.full;
     const long long threads =
         (long long)nsplit_tiles * TBM * ((EPI == EPI_SWIGLU ? TBN / 2 : TBN) / 4);
     hipLaunchKernelGGL((tile_fixup_kernel<EPI, TBM, TBN>), dim3((threads + 255) / 256),
                        dim3(256), 0, s, part, out, outf, M, N, mt, sp.full, nsplit_tiles,
-                       sp.tsplit);
+                       sp.tsplit, tmax, nt);
   }
 }
 
 template <int EPI, typename TB>
 void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N, int K,
                 f16 *out, float *outf, float *part, int mt, int nt, SplitPlan sp,
-                const acespec::RopeOut<TB> &ro = acespec::RopeOut<TB>{}) {
+                const acespec::RopeOut<TB> &ro = acespec::RopeOut<TB>{},
+                float *tmax = nullptr) {
   switch (var) {
-#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro); break;
+#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax); break;
     CASE(0) CASE(1) CASE(2) CASE(3)
 #undef CASE
     default: break;
@@ -711,7 +721,7 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
     hipLaunchKernelGGL(                                                                     \
         (gemm_f16w_kernel<EPI_RESID, bf16, g.wmn, g.wnn, g.wtm, g.wtn, g.nst, g.occ, g.kss>), \
         dim3(mt * nt * sp.tsplit), dim3(g.wmn * g.wnn * 64), 0, s, A, W, M, N, K, nullptr,   \
-        x, aux.part, mt, nt, 0, sp.tsplit, RopeOut<bf16>{});                                \
+        x, aux.part, mt, nt, 0, sp.tsplit, RopeOut<bf16>{}, nullptr);                       \
     launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
     break;                                                                                  \
   }
@@ -811,10 +821,11 @@ hipError_t launch_lm_head<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, 
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
   const SplitPlan sp =
       plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
-  if (sp.tsplit != 1 || tile_max == nullptr)
+  if (tile_max == nullptr || (sp.tsplit > 1 && (tbn / 4) > 64))
     return launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, logits, aux.part,
                                      aux.part_cap, aux.cus, s);
-  launch_epi<EPI_F32_MAX, bf16>(var, s, A, W, M, N, K, nullptr, logits, tile_max, mt, nt, sp);
+  launch_epi<EPI_F32_MAX, bf16>(var, s, A, W, M, N, K, nullptr, logits, aux.part, mt, nt, sp,
+                                RopeOut<bf16>{}, tile_max);
   *ntile = nt;
   return hipGetLastError();
 }
