@@ -138,6 +138,16 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   const int ntiles = (QR + 15) / 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
+  // With several tiles per wave, a last round of only a few tiles would leave the waves
+  // that hold one waiting at every chunk barrier for the waves that hold one more; each of
+  // those last rlast tiles is then split into 4 quarter units (one 16-key block of every
+  // chunk each), run in slot QS by the last 4 * rlast waves and merged through LDS.
+  constexpr int QS = UPW - 1;
+  const int rlast = ntiles - NW * QS;
+  const bool split_last = UPW > 1 && rlast >= 1 && 4 * rlast <= NW;
+  const int qbase = NW - 4 * rlast;  // first wave holding a quarter unit
+  const bool quarter = split_last && wave >= qbase;
+  const int qk = (wave - qbase) & 3;  // a quarter unit's key block within each chunk
   const int S = meta.sess_S[b];
   const int total = S + n1;
   const int nchunks = (total + KC - 1) / KC;
@@ -158,13 +168,14 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   f32x4 o[UPW][NB];
 #pragma unroll
   for (int t = 0; t < UPW; ++t) {
-    int qi = (wave + NW * t) * 16 + lr;
-    qi = qi < QR ? qi : QR - 1;
+    const int tile = (split_last && t == QS) ? NW * QS + ((wave - qbase) >> 2) : wave + NW * t;
+    int qi = tile * 16 + lr;   // (slot QS of a wave without a quarter unit: unused)
+    qi = qi < 0 ? 0 : (qi < QR ? qi : QR - 1);
     const int r = qi / G, h = g * G + (qi - r * G);
     const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
     // padding rows of the last tile multiply zeros (their outputs are dropped; zero
     // operands keep the MFMA's switching, and so its power draw, down)
-    const bool pad = (wave + NW * t) * 16 + lr >= QR;
+    const bool pad = tile * 16 + lr >= QR;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       const f16x8 v = *(const f16x8 *)(qp + s * 32 + lg * 8);
@@ -211,7 +222,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     const bool tree_chunk = key0 + KC > S;
 #pragma unroll
     for (int t = 0; t < UPW; ++t) {
-      if (wave + NW * t >= ntiles) break;
+      if (wave + NW * t >= ntiles || (split_last && t == QS)) break;
       // S^T for 4 blocks of 16 keys: sc[kk][e] is the score of slot
       // key0 + key_of_score(kk, lg, e) against this lane's query.
       f32x4 sc[4];
@@ -274,14 +285,128 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
           o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[ks], o[t][nb], 0, 0, 0);
         }
     }
+    if (quarter) {
+      // One 16-key block (key block qk of the chunk) of the split tile: 4 scores a lane.
+      f32x4 sq = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(key_of_row(qk, lr), s * 4 + lg));
+        sq = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[QS][s], sq, 0, 0, 0);
+      }
+      if (tree_chunk) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = key0 + key_of_score(qk, lg, e) - S;
+          const int sh = min(max(j - 1, 0), 63);
+          const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((anc[QS] >> sh) & 1ull)));
+          sq[e] = vis ? sq[e] : -INFINITY;
+        }
+      }
+      float mx = fmaxf(fmaxf(sq[0], sq[1]), fmaxf(sq[2], sq[3]));
+      mx = rows4_max(mx);
+      const float m_new = fmaxf(m_run[QS], mx);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f((m_run[QS] - m_use) * sscale);
+      m_run[QS] = m_new;
+      const float mb = m_use * sscale;
+      f16x4 pq;
+      float rs = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sq[e], sscale, -mb));
+        rs += p;
+        pq[e] = (f16)p;
+      }
+      l_run[QS] = l_run[QS] * alpha + rs;
+      if (__ballot(alpha < 1.f)) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[QS][nb][e] *= alpha;
+      }
+      // O^T += V^T P^T over the block's 16 keys: the lane's 4 probabilities are keys
+      // (qk/2)*32 + lg*8 + (qk%2)*4 + 0..3, half of one 16-byte V^T piece.
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const f16x4 va =
+            *(const f16x4 *)(sv + v_off(nb * 16 + lr, (qk >> 1) * 4 + lg) + (qk & 1) * 4);
+        o[QS][nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, pq, o[QS][nb], 0, 0, 0);
+      }
+    }
   }
   wait_vmcnt<0>();
+
+  if (split_last) {
+    // Merge the quarter units of each split tile (the ring is free once every wave is
+    // past its last chunk); each of a tile's 4 quarter waves finalises NB/4 head-dim blocks.
+    __syncthreads();
+    const int nquart = 4 * rlast;
+    f32x4 *mo = (f32x4 *)smem;                                  // [quarter][NB][64 lanes]
+    float *mml = (float *)smem + (size_t)nquart * NB * 64 * 4;  // [quarter][16 queries][2]
+    const int qu = wave - qbase;
+    if (quarter) {
+      const float l = rows4_sum(l_run[QS]);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) mo[(qu * NB + nb) * 64 + lane] = o[QS][nb];
+      if (lg == 0) {
+        mml[(qu * 16 + lr) * 2 + 0] = m_run[QS] == -INFINITY ? -INFINITY : m_run[QS] * sscale;
+        mml[(qu * 16 + lr) * 2 + 1] = l;
+      }
+    }
+    __syncthreads();
+    if (quarter) {
+      const int q0 = qu & ~3, tile = NW * QS + (qu >> 2);
+      float mj[4], wj[4];
+      float M = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        mj[j] = mml[((q0 + j) * 16 + lr) * 2];
+        M = fmaxf(M, mj[j]);
+      }
+      float L = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        wj[j] = mj[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mj[j] - M);
+        L += wj[j] * mml[((q0 + j) * 16 + lr) * 2 + 1];
+      }
+      const int qi = tile * 16 + lr;
+      if (qi < QR) {
+        const int r = qi / G, h = g * G + (qi - r * G);
+#pragma unroll
+        for (int i = 0; i < NB / 4; ++i) {
+          const int nb = qk * (NB / 4) + i;
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const f32x4 v = mo[((q0 + j) * NB + nb) * 64 + lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] += wj[j] * v[e];
+          }
+          if (nsplit == 1) {
+            const float inv = L > 0.f ? 1.0f / L : 0.f;
+            f16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (f16)(acc[e] * inv);
+            *(f16x4 *)(out + (row0 + r) * (size_t)q_stride + h * HD + nb * 16 + lg * 4) = v;
+          } else {
+            const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
+            *(f32x4 *)(part_o + (item * QR + qi) * HD + nb * 16 + lg * 4) = acc;
+          }
+        }
+        if (nsplit > 1 && qk == 0 && lg == 0) {
+          const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
+          part_ml[(item * QR + qi) * 2 + 0] = M;
+          part_ml[(item * QR + qi) * 2 + 1] = L;
+        }
+      }
+    }
+  }
 
   // o[t][nb][e] is head dim nb*16 + lg*4 + e of query tile*16 + lr.
 #pragma unroll
   for (int t = 0; t < UPW; ++t) {
     const int tile = wave + NW * t;
-    if (tile >= ntiles) break;
+    if (tile >= ntiles || (split_last && t == QS)) break;
     const float l = rows4_sum(l_run[t]);
     const int qi = tile * 16 + lr;
     if (qi >= QR) continue;
