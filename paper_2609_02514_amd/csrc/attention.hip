@@ -8,8 +8,10 @@
 //
 // bf16 model.  One workgroup of 16 waves (8 with more than 16 tiles) per (key split, kv
 // head, session).  Query rows are the G query heads of the kv head times the N+1 tree rows
-// (row = tree_row * G + head), in 16-row tiles dealt round-robin to the waves.  The key
-// range of the split streams through LDS in chunks of 64 slots:
+// (row = tree_row * G + head), in 16-row tiles dealt round-robin to the waves; with several
+// tiles per wave, a last round of at most NW/4 tiles is split into quarter units (one
+// 16-key block of every chunk each) on the waves that would otherwise idle, merged at the
+// end through LDS.  The key range of the split streams through LDS in chunks of 64 slots:
 //  * HBM -> LDS by direct DMA (global_load_lds, 16 bytes a lane) into a ring of NST
 //    stages.  A stage holds the chunk's keys as [64 slots][head_dim] and its values,
 //    read from the head-dim-major value cache, as [head_dim][64 slots].  The 16-byte
