@@ -6,14 +6,16 @@
 //   fp32 accumulation.  See the kernel comment below for the tiling and pipeline; tiles
 //   are ordered so that the row tiles of one weight panel land on the same XCD
 //   (workgroups are dealt round-robin over the 8 XCDs), which keeps that panel in one
-//   L2.  GEMMs whose tile count cannot fill the chip split K; the fp32 partials are
-//   summed in a fixed order (deterministic) by a small reduction kernel.
+//   L2.  Tiles of a last, partly empty round of workgroups (or every tile, when there
+//   are fewer tiles than workgroup slots) are sliced along K; the fp32 slices are summed
+//   in a fixed order (deterministic) by a fixup kernel that also applies the epilogue.
 // fp32 model (small models only): LDS-tiled FMA kernel with the same epilogues.
 //
-// Epilogues fuse the elementwise work that follows each product: fp32 store (QKV, LM
-// head), fp32 residual add (attention output and MLP down projections), SwiGLU
-// (gate/up projection: each tile holds matching gate and up columns), activation-type
-// store.
+// Epilogues fuse the elementwise work that follows each product: fp32 store (LM head,
+// with per-tile row maxima for the vocabulary kernel), RoPE + q store + cache write of
+// the tree K/V (QKV projection), fp32 residual add followed by the next block's RMSNorm
+// (attention output and MLP down projections), SwiGLU (gate/up projection: each tile
+// holds matching gate and up columns), activation-type store.
 #include <cmath>
 
 #include "common.h"
@@ -559,9 +561,11 @@ using acespec::EPI_F32_MAX;
 // the other loads), deeper rings (5-8 stages) at one workgroup per CU, with 64 x 64 wave
 // tiles or 128 x 512 block tiles, 128 x 128 tiles with 64-wide k stages, fp16 weights
 // (which only removes the in-register widening, worth 3-8 %), and weights and
-// activations pre-packed into 1 KB tile blocks (contiguous DMA; 2-9 %).  The limit of the 128 x 256 tiling is the L2 -> LDS path, not the MFMA
-// pipe: with the DMA removed it runs at 1.9 PFLOP/s, with the MFMAs removed at 75 % of
-// its full time.
+// activations pre-packed into 1 KB tile blocks (contiguous DMA; 2-9 %), 256 x 128 tiles,
+// and 256 x 256 tiles on 32 x 32 MFMAs with one wave per SIMD (128 x 128 wave tiles: the
+// single wave cannot cover the barrier and DMA waits).  Under load the part runs at a
+// power-limited 1.2-1.9 GHz shader clock on random operands, which every tiling here
+// meets at about the same rate.
 struct GemmVariant {
   int wmn, wnn, wtm, wtn, nst, occ, kss;
 };
