@@ -77,28 +77,34 @@ def _pmc_rows(run_dir):
 def _label_dispatches(rows):
     """Kernel kind of every dispatch of the verify library, from the symbol and the fixed
     launch order of a step (per layer: QKV, O, gate/up, down; LM head right before the
-    vocabulary kernel)."""
+    vocabulary kernel).  A K-slice fixup or RoPE dispatch that completes the product
+    launched just before it is labelled "+" (its bytes belong to that launch)."""
     labels, resid_seen = [], 0
     for i, r in enumerate(rows):
         n = r["Kernel_Name"]
         kind = None
         if "tree_attn_mfma_kernel" in n:
             kind = "tree_attention"
+        elif "attn_combine_kernel" in n or "tile_fixup_kernel" in n or \
+                "fixup_resid_norm_kernel" in n or "rope_kv_kernel" in n:
+            kind = "+"
         elif "gemm_f16w_kernelILi2E" in n:
             kind = "gemm_gate_up"
         elif "gemm_f16w_kernelILi1E" in n:
             kind = "gemm_o" if resid_seen % 2 == 0 else "gemm_down"
             resid_seen += 1
-        elif "gemm_f16w_kernelILi3E" in n:
+        elif "gemm_f16w_kernelILi4E" in n:          # QKV with its RoPE epilogue
+            kind = "gemm_qkv"
+        elif "gemm_f16w_kernelILi5E" in n:          # LM head with row maxima
+            kind = "gemm_lm_head"
+        elif "gemm_f16w_kernelILi3E" in n:          # fp32 store: QKV (sliced) or LM head
             nxt = next((rows[j]["Kernel_Name"] for j in range(i + 1, len(rows))
-                        if "splitk_reduce" not in rows[j]["Kernel_Name"]), "")
+                        if "fixup" not in rows[j]["Kernel_Name"]), "")
             kind = "gemm_lm_head" if "vocab_verify" in nxt else "gemm_qkv"
         elif "vocab_verify_kernel" in n:
             kind = "vocab_verify"
         elif "rmsnorm_kernel" in n:
             kind = "rmsnorm"
-        elif "rope_kv_kernel" in n:
-            kind = "rope_kv"
         labels.append(kind)
     return labels
 
@@ -115,11 +121,19 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mib
     acc = {}
     for which, d in (("fetch", fetch_dir), ("write", write_dir)):
         rows = _pmc_rows(d)
+        last = None   # (kind, index) of the last product launch
         for kind, r in zip(_label_dispatches(rows), rows):
+            v = float(r["Counter_Value"])
+            if kind == "+":
+                if last is not None:
+                    acc[last[0]][which][last[1]] += v
+                continue
             if kind is None:
+                last = None
                 continue
             e = acc.setdefault(kind, {"fetch": [], "write": []})
-            e[which].append(float(r["Counter_Value"]))
+            e[which].append(v)
+            last = (kind, len(e[which]) - 1)
     for kind, e in sorted(acc.items()):
         fk = sum(e["fetch"]) / max(len(e["fetch"]), 1)
         wk = sum(e["write"]) / max(len(e["write"]), 1)
