@@ -44,6 +44,8 @@ const char *kKindNames[K_COUNT] = {"tree_prep",    "embed",       "rmsnorm",
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
+constexpr int kCandCap = 4096;  // threshold-bin candidates kept per row (16 KB)
+
 }  // namespace
 
 struct acespec_ctx {
@@ -61,6 +63,7 @@ struct acespec_ctx {
   double *inv_freq = nullptr;
   float2 *rot = nullptr;      // RoPE (cos, sin) per tree row and frequency, per step
   float *tile_max = nullptr;  // LM-head row maxima per column tile
+  uint32_t *cand = nullptr;   // vocabulary kernel: threshold-bin candidates per row
   TreeMeta meta{};
   // timing
   bool timing = false;
@@ -187,6 +190,8 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   va.q_scalar = q_scalar;
   va.tile_max = ntile ? ctx->tile_max : nullptr;
   va.ntile = ntile;
+  va.cand = ctx->cand;
+  va.cand_cap = kCandCap;
   va.u = uniforms;
   va.tok = meta.tok;
   va.par = meta.par;
@@ -238,6 +243,8 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   va.q_scalar = nullptr;
   va.tile_max = ntile ? ctx->tile_max : nullptr;
   va.ntile = ntile;
+  va.cand = ctx->cand;
+  va.cand_cap = kCandCap;
   va.u = uniforms;
   va.tok = draft;
   va.par = nullptr;
@@ -308,7 +315,8 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->part_cap = layers ? ((long long)max_batch * d.n_kv_heads + 512) * QR * d.head_dim : 0;
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
-  void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr, *p_tmax = nullptr;
+  void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr, *p_tmax = nullptr,
+       *p_cand = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
@@ -320,6 +328,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       {layers ? R * d.d_ff * c->esz : 0, &c->h},
       {R * (size_t)d.vocab * 4, &p_logits},
       {R * (size_t)((d.vocab + 127) / 128) * 4, &p_tmax},
+      {R * (size_t)kCandCap * 4, &p_cand},
       {(size_t)c->part_cap * 4, &p_po},
       {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
       {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
@@ -355,6 +364,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->inv_freq = (double *)p_if;
   c->rot = (float2 *)p_rot;
   c->tile_max = (float *)p_tmax;
+  c->cand = (uint32_t *)p_cand;
   c->meta.tok = (int32_t *)p_tok;
   c->meta.par = (int32_t *)p_par;
   c->meta.pos = (int32_t *)p_pos;

@@ -246,6 +246,8 @@ struct VocabArgs {
   const float *q_scalar;    // [rows] q-hat of each row's own token, or NULL (dense mode)
   const float *tile_max;    // [rows, ntile] row maxima over column tiles, or NULL
   int ntile;
+  uint32_t *cand;           // [rows, cand_cap] scratch for threshold-bin candidates, or NULL
+  int cand_cap;
   const float *u;           // [rows, 3]
   const int32_t *tok;       // [rows] token of each row (children look theirs up here)
   const int32_t *par;       // [rows] parent row within the session, -1 for the root

@@ -61,6 +61,7 @@ struct VSmem {
   int32_t cand_id[KMAX];
   uint32_t cand_in[KMAX];
   uint32_t ncand;
+  uint32_t nbin;           // elements of the selected top-p / top-k bins (pass 2)
   // selection results
   u64 above_p;
   uint32_t above_k;
@@ -353,11 +354,15 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   select_bin<false>(sm, sm.h.cnt, sm.h.mass, 4096, K, 0, bk, ak);
 
   // ---- pass 2: refine bits 19..8 inside the selected bins ------------------------------
+  // The keys of those bins' elements also go to a per-row scratch list (kept in L2), so
+  // that pass 3 can read them instead of the row when they fit.
   for (int i = tid; i < 4096; i += VT) {
     sm.h.cnt[i] = 0;
     sm.h.mass[i] = 0;
     sm.h.cntk[i] = 0;
   }
+  if (tid == 0) sm.nbin = 0;
+  uint32_t *cl = a.cand ? a.cand + (size_t)row * a.cand_cap : nullptr;
   __syncthreads();
   for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
     float4 vv[VU];
@@ -375,6 +380,10 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
           atomicAdd(&sm.h.mass[mid], fixw(elem_e(zz[j], sel)));
         }
         if (hi == bk) atomicAdd(&sm.h.cntk[mid], 1u);
+        if (cl && (hi == bp || hi == bk)) {
+          const uint32_t slot = atomicAdd(&sm.nbin, 1u);
+          if (slot < (uint32_t)a.cand_cap) cl[slot] = key;
+        }
       }
     }
   }
@@ -392,7 +401,19 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     sm.h.mass[i] = 0;
     sm.h.cntk[i] = 0;
   }
+  const uint32_t nbin = sm.nbin;  // final: pass 2 ended with a barrier
   __syncthreads();
+  if (cl && nbin <= (uint32_t)a.cand_cap) {
+    // the candidates' keys (a key maps back to its logit exactly)
+    for (uint32_t i = tid; i < nbin; i += VT) {
+      const uint32_t key = cl[i];
+      if ((key >> 8) == pre_p) {
+        atomicAdd(&sm.h.cnt[key & 0xFF], 1u);
+        atomicAdd(&sm.h.mass[key & 0xFF], fixw(elem_e(key_to_f32(key), sel)));
+      }
+      if ((key >> 8) == pre_k) atomicAdd(&sm.h.cntk[key & 0xFF], 1u);
+    }
+  } else
   for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
     float4 vv[VU];
     load_step(z, V, i0, vv);
