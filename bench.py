@@ -53,7 +53,7 @@ CSRC = os.path.join(ROOT, "paper_2609_02514_amd", "csrc")
 KIND_SOURCES = {
     "tree_attention": ["attention.hip"], "gemm_qkv": ["gemm.hip"], "gemm_o": ["gemm.hip"],
     "gemm_gate_up": ["gemm.hip"], "gemm_down": ["gemm.hip"], "gemm_lm_head": ["gemm.hip"],
-    "vocab_verify": ["vocab.hip"], "rmsnorm": ["elementwise.hip"], "rope_kv": ["elementwise.hip"],
+    "vocab_verify": ["vocab.hip"], "rmsnorm": ["elementwise.hip"], "rope_table": ["elementwise.hip"],
 }
 
 

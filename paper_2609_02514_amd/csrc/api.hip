@@ -37,7 +37,7 @@ enum Kind {
   K_GEMM_DOWN, K_GEMM_LM, K_VOCAB, K_WALK, K_COMMIT, K_COUNT
 };
 const char *kKindNames[K_COUNT] = {"tree_prep",    "embed",       "rmsnorm",
-                                   "gemm_qkv",     "rope_kv",     "tree_attention",
+                                   "gemm_qkv",     "rope_table",  "tree_attention",
                                    "gemm_o",       "gemm_gate_up", "gemm_down",
                                    "gemm_lm_head", "vocab_verify", "path_walk",
                                    "commit_kv"};
