@@ -297,12 +297,14 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
 
   // Epilogue.  acc[i][j][e] is C[row = m0 + wm*WTM*16 + i*16 + lk*4 + e][col = .. + lr].
   if (ns > 1) {  // k-slice of a split tile: raw sums at [slice][tile row][W-tile row]
+    // (rows past M are never read back)
     float *pt = part + ((size_t)(tile - full) * ns + sp) * (TBM * TBN);
 #pragma unroll
     for (int ii = 0; ii < WTM; ++ii)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int lrow = wm * WTM * 16 + ii * 16 + lk * 4 + e;
+        if (m0 + lrow >= M) continue;
 #pragma unroll
         for (int j = 0; j < WTN; ++j) {
           const int tc = (EPI == acespec::EPI_SWIGLU)
@@ -386,10 +388,11 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
   const int lrow = rem / CW, c4 = (rem - lrow * CW) * 4;
   const int tile = full + t, tn = tile / mt, tm = tile - tn * mt;
   const int row = tm * TBM + lrow;
+  // rows past M have no partials; with the row maxima their lanes still join the shuffles
   if (EPI != acespec::EPI_F32_MAX && row >= M) return;
   const float *pt = part + (size_t)t * tsplit * (TBM * TBN) + (size_t)lrow * TBN + c4;
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f), g = a;
-  for (int sp = 0; sp < tsplit; ++sp) {
+  for (int sp = 0; sp < (row < M ? tsplit : 0); ++sp) {
     const float4 v = *(const float4 *)(pt + (size_t)sp * (TBM * TBN));
     a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
     if (EPI == acespec::EPI_SWIGLU) {
