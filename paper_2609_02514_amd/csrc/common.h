@@ -40,8 +40,9 @@ AS_DEVICE f16x8 bf16x8_to_f16x8(bf16x8 v) {
 
 // Order-preserving map of an fp32 value to uint32 (larger float -> larger key).
 AS_DEVICE uint32_t f32_key(float f) {
-  uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  const uint32_t u = __float_as_uint(f);
+  // negative: all bits flipped; otherwise the sign bit set
+  return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 
 AS_DEVICE float wave_max(float v) {

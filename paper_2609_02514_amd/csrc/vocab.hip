@@ -165,7 +165,11 @@ struct Sel {
   float invSN;             // 1 / nucleus mass (fixed point units)
 };
 
-AS_DEVICE float elem_e(float z, const Sel &s) { return exp2f((z - s.M) * s.c); }
+// The raw v_exp_f32: for exponents >= -126 it is exactly exp2f (whose extra steps only
+// rescale subnormal results), and anything below 2^-41 rounds to 0 in fixed point anyway.
+AS_DEVICE float elem_e(float z, const Sel &s) {
+  return __builtin_amdgcn_exp2f((z - s.M) * s.c);
+}
 
 // p_r of one element given its nucleus membership.
 AS_DEVICE float elem_p(float z, bool in, const Sel &s) {
