@@ -69,6 +69,9 @@ struct VSmem {
 };
 
 AS_DEVICE u64 fixw(float v) { return __float2ull_rn(v * AS_FX_SCALE); }
+// fixw(v) as a float, exactly: for v <= 1 the product is at most 2^40, and either it is
+// already an integer (>= 2^23) or its rounding is below 2^24, so the value is representable.
+AS_DEVICE float fixw_f(float v) { return rintf(v * AS_FX_SCALE); }
 
 AS_DEVICE float key_to_f32(uint32_t key) {  // inverse of f32_key
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
@@ -173,7 +176,7 @@ AS_DEVICE float elem_e(float z, const Sel &s) {
 
 // p_r of one element given its nucleus membership.
 AS_DEVICE float elem_p(float z, bool in, const Sel &s) {
-  return in ? (float)fixw(elem_e(z, s)) * s.invSN : 0.f;
+  return in ? fixw_f(elem_e(z, s)) * s.invSN : 0.f;
 }
 
 // Nucleus / top-k membership given the element's rank among ids tied at the threshold.
