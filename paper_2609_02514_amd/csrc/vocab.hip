@@ -283,18 +283,38 @@ AS_DEVICE int find_segment(const u64 *excl, int nseg, u64 target) {
   return lo;
 }
 
-// Loads the VU float4 this thread handles in one step of a pass over the row (-inf past
-// the end), all issued before any is used: one load in flight per thread leaves the
-// passes bound by memory latency rather than bandwidth.
+// Loads the VU float4 this thread handles in one step of a pass over the row, all issued
+// before any is used: one load in flight per thread leaves the passes bound by memory
+// latency rather than bandwidth.  Past the end of the row the row's last float4 is
+// loaded again (V is a multiple of 4): every load is unconditional, so the compiler can
+// wait for the older loads only, and the callers skip those entries (or, for the row
+// maximum, take them: they repeat real elements).
 constexpr int VU = 4;
 AS_DEVICE void load_step(const float *z, int V, int i0, float4 (&v)[VU]) {
 #pragma unroll
   for (int u = 0; u < VU; ++u) {
     const int i = i0 + u * VT * 4;
-    v[u] = i < V ? *(const float4 *)(z + i)
-                 : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    v[u] = *(const float4 *)(z + (i < V ? i : V - 4));
   }
 }
+
+// A pass over the row, VU float4 per thread a step: the next step's loads are issued
+// before the current step is processed, so a thread always has loads in flight.
+struct RowStream {
+  const float *z;
+  int V, i0;
+  float4 cur[VU], nxt[VU];
+  AS_DEVICE RowStream(const float *z_, int V_, int start) : z(z_), V(V_), i0(start) {
+    load_step(z, V, i0, cur);
+  }
+  AS_DEVICE bool more() const { return i0 < V; }
+  AS_DEVICE void prefetch() { load_step(z, V, i0 + VT * 4 * VU, nxt); }
+  AS_DEVICE void advance() {
+#pragma unroll
+    for (int u = 0; u < VU; ++u) cur[u] = nxt[u];
+    i0 += VT * 4 * VU;
+  }
+};
 
 __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) {
   __shared__ VSmem sm;
@@ -310,9 +330,10 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     const float *tm = a.tile_max + (size_t)row * a.ntile;
     for (int t = tid; t < a.ntile; t += VT) mx = fmaxf(mx, tm[t]);
   } else {
-    for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
-      float4 vv[VU];
-      load_step(z, V, i0, vv);
+    for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
+      rs.prefetch();
+      const int i0 = rs.i0;
+      const float4 (&vv)[VU] = rs.cur;
 #pragma unroll
       for (int u = 0; u < VU; ++u)
         mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
@@ -331,9 +352,10 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   if (tid == 0) sm.ncand = 0;
   __syncthreads();
   u64 tot = 0;
-  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
-    float4 vv[VU];
-    load_step(z, V, i0, vv);
+  for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
+    rs.prefetch();
+    const int i0 = rs.i0;
+    const float4 (&vv)[VU] = rs.cur;
 #pragma unroll
     for (int u = 0; u < VU; ++u) {
       if (i0 + u * VT * 4 >= V) break;
@@ -371,9 +393,10 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   if (tid == 0) sm.nbin = 0;
   uint32_t *cl = a.cand ? a.cand + (size_t)row * a.cand_cap : nullptr;
   __syncthreads();
-  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
-    float4 vv[VU];
-    load_step(z, V, i0, vv);
+  for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
+    rs.prefetch();
+    const int i0 = rs.i0;
+    const float4 (&vv)[VU] = rs.cur;
 #pragma unroll
     for (int u = 0; u < VU; ++u) {
       if (i0 + u * VT * 4 >= V) break;
@@ -421,9 +444,10 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
       if ((key >> 8) == pre_k) atomicAdd(&sm.h.cntk[key & 0xFF], 1u);
     }
   } else
-  for (int i0 = tid * 4; i0 < V; i0 += VT * 4 * VU) {
-    float4 vv[VU];
-    load_step(z, V, i0, vv);
+  for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
+    rs.prefetch();
+    const int i0 = rs.i0;
+    const float4 (&vv)[VU] = rs.cur;
 #pragma unroll
     for (int u = 0; u < VU; ++u) {
       if (i0 + u * VT * 4 >= V) break;
