@@ -538,19 +538,22 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   const bool dense_q = a.q_scalar == nullptr;
   const bool resid = has_child && dense_q;
   const float *q = dense_q ? a.q + (size_t)row * V : nullptr;
-  for (int s0 = wave; s0 < nseg; s0 += NWV * VU) {
-  // the VU segments of this step are loaded before any is used
-  float4 z4u[VU], q4u[VU];
+  // The VU segments of a step are loaded before any is used, and the next step's loads
+  // are issued before the current step is processed.  Past the end of the row the last
+  // float4 is loaded again (unconditional loads); those lanes are not valid below.
+  auto seg_load = [&](int s0_, float4 (&zl)[VU], float4 (&ql)[VU]) {
 #pragma unroll
-  for (int u = 0; u < VU; ++u) {
-    const int id0 = (s0 + u * NWV) * SEG + lane * 4;
-    z4u[u] = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-    q4u[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (s0 + u * NWV < nseg && id0 < V) {
-      z4u[u] = *(const float4 *)(z + id0);
-      if (resid) q4u[u] = *(const float4 *)(q + id0);
+    for (int u = 0; u < VU; ++u) {
+      const int id0 = (s0_ + u * NWV) * SEG + lane * 4;
+      const int ld = id0 < V ? id0 : V - 4;
+      zl[u] = *(const float4 *)(z + ld);
+      ql[u] = resid ? *(const float4 *)(q + ld) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-  }
+  };
+  float4 z4u[VU], q4u[VU], z4n[VU], q4n[VU];
+  seg_load(wave, z4u, q4u);
+  for (int s0 = wave; s0 < nseg; s0 += NWV * VU) {
+  seg_load(s0 + NWV * VU, z4n, q4n);
 #pragma unroll
   for (int u = 0; u < VU; ++u) {
     const int s = s0 + u * NWV;
@@ -596,6 +599,11 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
       sm.g.seg_p[s] = sp_;
       sm.g.seg_r[s] = sr_;
     }
+  }
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    z4u[u] = z4n[u];
+    q4u[u] = q4n[u];
   }
   }
   __syncthreads();
