@@ -549,12 +549,13 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
 #define GO(HD_, NW_, UPW_)                                                                \
   launch_mfma<HD_, NW_, UPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,  \
                               capacity, nsplit)
+  // (more than 16 tiles means at least 3 a wave)
   if (hd == 128) {
     if (nw == 16) GO(128, 16, 1);
-    else if (upw == 2) GO(128, 8, 2); else if (upw == 3) GO(128, 8, 3); else GO(128, 8, 4);
+    else if (upw == 3) GO(128, 8, 3); else GO(128, 8, 4);
   } else {
     if (nw == 16) GO(64, 16, 1);
-    else if (upw == 2) GO(64, 8, 2); else if (upw == 3) GO(64, 8, 3); else GO(64, 8, 4);
+    else if (upw == 3) GO(64, 8, 3); else GO(64, 8, 4);
   }
 #undef GO
   hipError_t e = hipGetLastError();
