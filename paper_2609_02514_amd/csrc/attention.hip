@@ -208,6 +208,19 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     if (widener) widen_chunk<HD>(stage_of(c0), wt, wstride, c0 * KC, total);
   }
 
+  // Fragment offsets: the swizzles depend on the lane only, so the read of K block kk at
+  // k-step s is koff[s] + key_of_row(kk, 0) * HD and that of V^T block nb at key step ks is
+  // voff[ks] + nb * 16 * KC -- a few lane registers plus compile-time constants.
+  const int ksw_l = ksw<HD>(key_of_row(0, lr));
+  int koff[KSTEPS], voff[2];
+#pragma unroll
+  for (int s = 0; s < KSTEPS; ++s)
+    koff[s] = key_of_row(0, lr) * HD + (((s * 4 + lg) ^ ksw_l) << 3);
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) voff[ks] = v_off(lr, ks * 4 + lg);
+  const int qkoff = key_of_row(qk, 0) * HD;                   // quarter: its key block
+  const int qvoff = (qk & 2 ? voff[1] : voff[0]) + (qk & 1) * 4;  // and its V^T half-piece
+
   for (int c = c0; c < c1; ++c) {
     if (c + 1 < c1) {
       if (c + NST - 2 < c1) wait_vmcnt<(NST - 3) * L_DMA>(); else wait_vmcnt<0>();
@@ -234,7 +247,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       for (int s = 0; s < KSTEPS; ++s)
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(key_of_row(kk, lr), s * 4 + lg));
+          const f16x8 kf = *(const f16x8 *)(sk + koff[s] + key_of_row(kk, 0) * HD);
           sc[kk] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[kk], 0, 0, 0);
         }
       if (tree_chunk) {
@@ -283,7 +296,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          const f16x8 va = *(const f16x8 *)(sv + v_off(nb * 16 + lr, ks * 4 + lg));
+          const f16x8 va = *(const f16x8 *)(sv + voff[ks] + nb * 16 * KC);
           o[t][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[ks], o[t][nb], 0, 0, 0);
         }
     }
@@ -292,7 +305,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       f32x4 sq = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
-        const f16x8 kf = *(const f16x8 *)(sk + k_off<HD>(key_of_row(qk, lr), s * 4 + lg));
+        const f16x8 kf = *(const f16x8 *)(sk + koff[s] + qkoff);
         sq = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[QS][s], sq, 0, 0, 0);
       }
       if (tree_chunk) {
@@ -330,8 +343,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       // (qk/2)*32 + lg*8 + (qk%2)*4 + 0..3, half of one 16-byte V^T piece.
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const f16x4 va =
-            *(const f16x4 *)(sv + v_off(nb * 16 + lr, (qk >> 1) * 4 + lg) + (qk & 1) * 4);
+        const f16x4 va = *(const f16x4 *)(sv + qvoff + nb * 16 * KC);
         o[QS][nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, pq, o[QS][nb], 0, 0, 0);
       }
     }
