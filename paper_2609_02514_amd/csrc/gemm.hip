@@ -228,11 +228,23 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     // 64-row parts so that each head's rotation pairs (i, i + hd/2) and each value
     // column's run of consecutive tree slots can be read across waves.
     constexpr int CR = 64, SP = TBN + 4;  // rows per part, row pitch in floats
-    static_assert(CR * SP * 4 <= NST * STAGE_BYTES, "a part of the tile fits the ring");
+    static_assert(CR * SP * 4 + CR * 8 <= NST * STAGE_BYTES,
+                  "a part of the tile and its row table fit the ring");
     float *st = (float *)smem;
+    int *rsess = (int *)(st + CR * SP);  // per row of the part: its session,
+    int *rslot = rsess + CR;             // and the cache slot of its tree row
     const int hd = ro.hd, half = hd >> 1, nheads = ro.H + 2 * ro.Hkv;
+    const int lq4 = hd == 128 ? 4 : 3;  // log2 of the 4-frequency items per row (hd 64 or 128)
     for (int c0 = 0; c0 < TBM; c0 += CR) {
       __syncthreads();  // every wave is past the ring / the previous part
+      if (tid < CR) {
+        const int row = m0 + c0 + tid;
+        if (row < M) {
+          const int b = row / ro.n1;
+          rsess[tid] = b;
+          rslot[tid] = ro.sess_S[b] + row - b * ro.n1;
+        }
+      }
 #pragma unroll
       for (int ii = 0; ii < WTM; ++ii)
 #pragma unroll
@@ -248,9 +260,8 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
         if (gh >= nheads) break;
         const float *sb = st + hb * hd;
         if (gh < ro.H + ro.Hkv) {  // query or key head: rotate-half, 4 frequencies a thread
-          const int q4 = half >> 2;
-          for (int it = tid; it < CR * q4; it += NW * 64) {
-            const int r = it / q4, i = (it - r * q4) * 4, row = m0 + c0 + r;
+          for (int it = tid; it < (CR << lq4); it += NW * 64) {
+            const int r = it >> lq4, i = (it & ((1 << lq4) - 1)) * 4, row = m0 + c0 + r;
             if (row >= M) continue;
             const float4 a1 = *(const float4 *)(sb + r * SP + i);
             const float4 a2 = *(const float4 *)(sb + r * SP + i + half);
@@ -271,9 +282,8 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
               *(h4 *)(qo + i + half) = h4{(f16)y2[0], (f16)y2[1], (f16)y2[2], (f16)y2[3]};
             } else {
               typedef TB t4 __attribute__((ext_vector_type(4)));
-              const int b = row / ro.n1, rr = row - b * ro.n1;
-              TB *kd = ro.ck + (((size_t)b * ro.Hkv + (gh - ro.H)) * ro.capacity +
-                                ro.sess_S[b] + rr) * hd;
+              TB *kd = ro.ck + (((size_t)rsess[r] * ro.Hkv + (gh - ro.H)) * ro.capacity +
+                                rslot[r]) * hd;
               *(t4 *)(kd + i) = t4{from_f32<TB>(y1[0]), from_f32<TB>(y1[1]),
                                    from_f32<TB>(y1[2]), from_f32<TB>(y1[3])};
               *(t4 *)(kd + i + half) = t4{from_f32<TB>(y2[0]), from_f32<TB>(y2[1]),
@@ -285,8 +295,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
           for (int it = tid; it < CR * hd; it += NW * 64) {
             const int dd = it / CR, r = it - dd * CR, row = m0 + c0 + r;
             if (row >= M) continue;
-            const int b = row / ro.n1, rr = row - b * ro.n1;
-            ro.cv[(((size_t)b * ro.Hkv + g) * hd + dd) * ro.capacity + ro.sess_S[b] + rr] =
+            ro.cv[(((size_t)rsess[r] * ro.Hkv + g) * hd + dd) * ro.capacity + rslot[r]] =
                 from_f32<TB>(sb[r * SP + dd]);
           }
         }
