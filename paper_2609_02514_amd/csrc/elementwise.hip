@@ -94,10 +94,11 @@ __global__ void rope_table_kernel(const int32_t *__restrict__ pos,
   rot[idx] = make_float2((float)cd, (float)sd);
 }
 
-// grid: (kv heads, sessions); block: 1024 threads.  One block rotates the session's tree
-// rows for one kv head and the G query heads that share it, so that its value columns
-// land as runs of consecutive slots in the head-dim-major value cache.
-constexpr int ROPE_MAX_ROWS = 65, ROPE_MAX_HALF = 64, ROPE_THREADS = 1024;
+// grid: (kv heads, sessions, chunks of ROPE_ROWS tree rows); block: 256 threads.  One block
+// rotates ROPE_ROWS tree rows of one session for one kv head and the G query heads that
+// share it, so that its value columns land as runs of consecutive slots in the
+// head-dim-major value cache.
+constexpr int ROPE_ROWS = 16, ROPE_MAX_HALF = 64, ROPE_THREADS = 256;
 template <typename TW, typename TA>
 __global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__restrict__ qkv,
                                                       TA *__restrict__ q_out, TreeMeta meta,
@@ -105,40 +106,59 @@ __global__ __launch_bounds__(ROPE_THREADS) void rope_kv_kernel(const float *__re
                                                       int n1, int H, int Hkv, int hd,
                                                       int capacity,
                                                       const float2 *__restrict__ rot) {
-  __shared__ float vs[ROPE_MAX_ROWS * (2 * ROPE_MAX_HALF + 1)];
-  const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  __shared__ float vs[ROPE_ROWS * (2 * ROPE_MAX_HALF + 1)];
+  const int g = blockIdx.x, b = blockIdx.y, r0 = blockIdx.z * ROPE_ROWS, tid = threadIdx.x;
+  const int nr = min(ROPE_ROWS, n1 - r0);  // rows of this block
   const int half = hd >> 1, G = H / Hkv;
+  // item e of a row-major [nr][half] walk -> (row, frequency); shifts when half is a power
+  // of two (every bf16 model: head_dim 64 or 128)
+  const bool pow2 = (half & (half - 1)) == 0;
+  const int lh = __builtin_ctz(half);
+  auto split = [&](int e, int &r, int &i) {
+    if (pow2) { r = e >> lh; i = e & (half - 1); }
+    else { r = e / half; i = e - r * half; }
+  };
   const size_t W = (size_t)(H + 2 * Hkv) * hd;  // qkv row width
-  const float *base = qkv + (size_t)b * n1 * W;
-  const float2 *rt = rot + (size_t)b * n1 * half;
-  for (int e = tid; e < n1 * hd; e += ROPE_THREADS) {  // this head's values, row-major
-    const int r = e / hd, dd = e - r * hd;
+  const float *base = qkv + ((size_t)b * n1 + r0) * W;
+  const float2 *rt = rot + ((size_t)b * n1 + r0) * half;
+  for (int e = tid; e < nr * hd; e += ROPE_THREADS) {  // this head's values, row-major
+    int r, i;
+    split(e >> 1, r, i);                 // (two items of a row per frequency)
+    const int dd = e - r * hd;
     vs[r * (hd + 1) + dd] = base[r * W + (size_t)(H + Hkv + g) * hd + dd];
   }
   __syncthreads();
-  for (int e = tid; e < n1 * G * half; e += ROPE_THREADS) {  // queries
-    const int i = e % half, t = e / half, hh = t % G, r = t / G;
+  for (int hh = 0; hh < G; ++hh) {  // queries, one head of the group at a time
     const int h = g * G + hh;
-    const float *x = base + r * W + (size_t)h * hd;
-    const float2 cs = rt[r * half + i];
-    const float x1 = x[i], x2 = x[i + half];
-    TA *qo = q_out + ((size_t)b * n1 + r) * H * hd + (size_t)h * hd;
-    qo[i] = from_f32<TA>(x1 * cs.x - x2 * cs.y);
-    qo[i + half] = from_f32<TA>(x2 * cs.x + x1 * cs.y);
+    for (int e = tid; e < nr * half; e += ROPE_THREADS) {
+      int r, i;
+      split(e, r, i);
+      const float *x = base + r * W + (size_t)h * hd;
+      const float2 cs = rt[e];
+      const float x1 = x[i], x2 = x[i + half];
+      TA *qo = q_out + ((size_t)b * n1 + r0 + r) * H * hd + (size_t)h * hd;
+      qo[i] = from_f32<TA>(x1 * cs.x - x2 * cs.y);
+      qo[i + half] = from_f32<TA>(x2 * cs.x + x1 * cs.y);
+    }
   }
   const int S = meta.sess_S[b];
-  for (int e = tid; e < n1 * half; e += ROPE_THREADS) {  // keys
-    const int i = e % half, r = e / half;
+  for (int e = tid; e < nr * half; e += ROPE_THREADS) {  // keys
+    int r, i;
+    split(e, r, i);
     const float *k = base + r * W + (size_t)(H + g) * hd;
     const float2 cs = rt[e];
     const float x1 = k[i], x2 = k[i + half];
-    const size_t kdst = (((size_t)b * Hkv + g) * capacity + S + r) * hd;
+    const size_t kdst = (((size_t)b * Hkv + g) * capacity + S + r0 + r) * hd;
     ck[kdst + i] = from_f32<TW>(x1 * cs.x - x2 * cs.y);
     ck[kdst + i + half] = from_f32<TW>(x2 * cs.x + x1 * cs.y);
   }
-  for (int e = tid; e < hd * n1; e += ROPE_THREADS) {  // values: consecutive threads, consecutive slots
-    const int dd = e / n1, r = e - dd * n1;
-    cv[(((size_t)b * Hkv + g) * hd + dd) * capacity + S + r] = from_f32<TW>(vs[r * (hd + 1) + dd]);
+  // values: runs of ROPE_ROWS consecutive slots per head dim (consecutive threads,
+  // consecutive slots)
+  for (int e = tid; e < hd * ROPE_ROWS; e += ROPE_THREADS) {
+    const int dd = e / ROPE_ROWS, r = e % ROPE_ROWS;
+    if (r < nr)
+      cv[(((size_t)b * Hkv + g) * hd + dd) * capacity + S + r0 + r] =
+          from_f32<TW>(vs[r * (hd + 1) + dd]);
   }
 }
 
@@ -186,9 +206,9 @@ template <typename TW>
 hipError_t launch_rope_kv(const float *qkv, typename ActOf<TW>::type *q_out,
                           const TreeMeta &meta, TW *cache_k, TW *cache_v, int B, int n1, int H,
                           int Hkv, int hd, int capacity, const float2 *rot, hipStream_t s) {
-  if (n1 > ROPE_MAX_ROWS || hd > 2 * ROPE_MAX_HALF || H % Hkv) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>), dim3(Hkv, B),
-                     dim3(ROPE_THREADS),
+  if (hd > 2 * ROPE_MAX_HALF || H % Hkv) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((rope_kv_kernel<TW, typename ActOf<TW>::type>),
+                     dim3(Hkv, B, (n1 + ROPE_ROWS - 1) / ROPE_ROWS), dim3(ROPE_THREADS),
                      0, s, qkv, q_out, meta, cache_k, cache_v, n1, H, Hkv, hd, capacity, rot);
   return hipGetLastError();
 }
