@@ -144,9 +144,9 @@ int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *weights,
                         const float *uniforms, int B, int N, const acespec_params *params,
                         const acespec_outputs *outs, hipStream_t stream);
 
-/* The same step for the paper's own uplink (Section III-B: the edge sends the drafted
- * tokens and a compressed draft distribution, Algorithm 1 line 3; the cloud "skips token
- * resampling" and returns the rejection index with a sparse target distribution):
+/* The same step for the paper's own uplink (Section III-B, Algorithm 1: the edge sends
+ * the drafted tokens and a compressed draft distribution; the cloud does no resampling of
+ * its own and returns the rejection index with a sparse target distribution):
  *  q_hat [B, N+1] fp32: q_hat[b, r] = the draft probability of row r's own token under
  *                its parent's draft distribution (row 0 unused) -- one float per node
  *                instead of a vocabulary-sized row.

@@ -18,7 +18,7 @@ the output law stays that of the target model):
       (of p_r itself if that residual has no mass)
   V6  acc_prefix_len[n] = leading accepted nodes on the root-to-n path
 
-Walk (Algorithm 1, lines 6-10): from the root follow the main (lowest-index)
+Walk (Algorithm 1, after verification): from the root follow the main (lowest-index)
 child while accepted; on a rejection the resampled token is looked up among
 the other children (w = (pi, x_resampled) in dom(T)); a hit continues down
 that sibling, a miss ends the path with the resampled token; a node without
@@ -161,7 +161,7 @@ class WalkResult:
 
 
 def walk(tokens: Sequence[int], parents: Sequence[int], res: RowResult) -> WalkResult:
-    """Algorithm 1, lines 6-10, on the GPU-side verification results of one tree."""
+    """The walk of Algorithm 1 on the GPU-side verification results of one tree."""
     ch = children_of(parents)
     cur, path, hit = 0, [], False
     while True:
@@ -233,7 +233,7 @@ def walk_tail(accept: np.ndarray, resample: np.ndarray, chain_len: int):
 
 def accept_scalar(p: np.ndarray, x: int, q_hat: float, u0: float) -> bool:
     """Acceptance of a drafted token from its draft probability alone (the uplink carries
-    q(x) per drafted token, Algorithm 1 line 3): accept iff u0 * q_hat < p(x)."""
+    q(x) per drafted token, Algorithm 1): accept iff u0 * q_hat < p(x)."""
     return bool(u0 * q_hat < p[x])
 
 

@@ -1,4 +1,4 @@
-// Per-session path walk over the verification results (Algorithm 1, lines 6-10).
+// Per-session path walk over the verification results (Algorithm 1: the walk after verification).
 //
 // From the root, follow the main (lowest-index) child while it is accepted.  When the
 // main child is rejected, its residual resample is looked up among the other children

@@ -1,5 +1,5 @@
 """GPU parity of the paper's own protocol (scalar q-hat uplink, no cloud-side sampling,
-edge-side resampling from the k-sparse payload; Section III-B, Algorithm 1 lines 3-7)."""
+edge-side resampling from the k-sparse payload; Section III-B, Algorithm 1)."""
 import numpy as np
 import pytest
 import torch

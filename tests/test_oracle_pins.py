@@ -9,7 +9,7 @@
   numpy's searchsorted, the exactness theorem of speculative sampling (output law == the
   target law, Chen et al., cited in Section II) driven through the oracle's own code on
   a midpoint grid, and a Monte Carlo law check of the walk with sibling hits
-  (Algorithm 1, lines 6-10).
+  (Algorithm 1).
 """
 import json
 import os

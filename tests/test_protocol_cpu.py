@@ -1,5 +1,5 @@
 """The paper's own protocol (scalar q-hat uplink, k-sparse downlink, edge-side resampling,
-Algorithm 1 lines 3-7): pins of the oracle's reading, and the edge resampler (product code,
+Algorithm 1): pins of the oracle's reading, and the edge resampler (product code,
 CPU by design) against it."""
 import numpy as np
 import pytest
