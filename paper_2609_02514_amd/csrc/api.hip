@@ -208,7 +208,8 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   va.topk_ids = o->topk_ids;
   va.topk_probs = o->topk_probs;
   RUN(K_VOCAB, launch_vocab(va, stream));
-  RUN(K_WALK, launch_walk(meta.tok, meta.par, o->accept, o->resample_token, o->bonus_token, B,
+  RUN(K_WALK, launch_walk(meta.tok, meta.par, meta.depth, o->accept, o->resample_token,
+                          o->bonus_token, B,
                           n1, o->acc_prefix_len, o->path, o->path_len, o->next_token,
                           o->sibling_hit, stream));
   return ACESPEC_OK;

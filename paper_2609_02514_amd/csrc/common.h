@@ -264,8 +264,9 @@ struct VocabArgs {
 };
 hipError_t launch_vocab(const VocabArgs &a, hipStream_t s);
 
-hipError_t launch_walk(const int32_t *tok, const int32_t *par, const uint8_t *accept,
-                       const int32_t *resample, const int32_t *bonus, int B, int n1,
+hipError_t launch_walk(const int32_t *tok, const int32_t *par, const int32_t *depth,
+                       const uint8_t *accept, const int32_t *resample, const int32_t *bonus,
+                       int B, int n1,
                        int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
                        int32_t *next_token, uint8_t *sibling_hit, hipStream_t s);
 

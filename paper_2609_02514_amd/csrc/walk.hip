@@ -10,44 +10,66 @@
 
 namespace {
 
-constexpr int MAXN1 = 65;
+constexpr int WALK_THREADS = 128;  // one thread per tree row (at most 65 rows)
 
-__global__ void walk_kernel(const int32_t *__restrict__ tok, const int32_t *__restrict__ par,
-                            const uint8_t *__restrict__ accept,
-                            const int32_t *__restrict__ resample,
-                            const int32_t *__restrict__ bonus, int B, int n1,
-                            int32_t *__restrict__ acc_prefix_len, int32_t *__restrict__ path,
-                            int32_t *__restrict__ path_len, int32_t *__restrict__ next_token,
-                            uint8_t *__restrict__ sibling_hit) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= B) return;
+// One workgroup per session.  Leading accepted nodes of row r's root-to-r path:
+// min(depth[r], f[r] - 1), f[r] the depth of the shallowest rejected node on the path
+// (the root is never tested), folded in by pointer jumping over the parents (7 rounds
+// cover 65 rows).  The walk itself then runs on one thread over the session's data in
+// LDS, with each node's main child found beforehand by an LDS minimum.
+__global__ __launch_bounds__(WALK_THREADS) void walk_kernel(
+    const int32_t *__restrict__ tok, const int32_t *__restrict__ par,
+    const int32_t *__restrict__ depth, const uint8_t *__restrict__ accept,
+    const int32_t *__restrict__ resample, const int32_t *__restrict__ bonus, int B, int n1,
+    int32_t *__restrict__ acc_prefix_len, int32_t *__restrict__ path,
+    int32_t *__restrict__ path_len, int32_t *__restrict__ next_token,
+    uint8_t *__restrict__ sibling_hit) {
+  constexpr int NONE = 1 << 30;
+  __shared__ int s_par[WALK_THREADS], s_tok[WALK_THREADS], s_rs[WALK_THREADS];
+  __shared__ int s_bonus[WALK_THREADS], s_main[WALK_THREADS], s_jump[WALK_THREADS];
+  __shared__ int s_f[WALK_THREADS];
+  __shared__ uint8_t s_acc[WALK_THREADS];
+  const int b = blockIdx.x, r = threadIdx.x;
   const size_t base = (size_t)b * n1;
-  int depth[MAXN1], acc[MAXN1];
-  depth[0] = 0;
-  acc[0] = 0;
-  acc_prefix_len[base] = 0;
-  for (int r = 1; r < n1; ++r) {
-    const int p = par[base + r];
-    depth[r] = depth[p] + 1;
-    const bool full = acc[p] == depth[p];
-    acc[r] = (full && accept[base + r]) ? acc[p] + 1 : acc[p];
-    acc_prefix_len[base + r] = acc[r];
+  const bool in = r < n1;
+  const int p = in ? par[base + r] : -1;
+  const int d = in ? depth[base + r] : 0;
+  const bool ok = r == 0 || !in || accept[base + r] != 0;
+  s_par[r] = p;
+  s_tok[r] = in ? tok[base + r] : -1;
+  s_rs[r] = in ? resample[base + r] : -1;
+  s_bonus[r] = in ? bonus[base + r] : -1;
+  s_acc[r] = ok ? 1 : 0;
+  s_main[r] = NONE;
+  s_jump[r] = p < 0 ? 0 : p;
+  s_f[r] = ok ? NONE : d;
+  __syncthreads();
+  if (p >= 0) atomicMin(&s_main[p], r);
+  for (int round = 0; round < 7; ++round) {
+    __syncthreads();
+    const int jr = s_jump[r];
+    const int f = min(s_f[r], s_f[jr]);
+    const int jj = s_jump[jr];
+    __syncthreads();
+    s_f[r] = f;
+    s_jump[r] = jj;
   }
+  if (in) acc_prefix_len[base + r] = min(d, s_f[r] - 1);
+  __syncthreads();  // main children complete
+  if (r != 0) return;
   int cur = 0, len = 0, hit = 0, nxt = -1;
-  while (true) {
-    int main_c = -1;
-    for (int c = cur + 1; c < n1; ++c)
-      if (par[base + c] == cur) { main_c = c; break; }
-    if (main_c < 0) { nxt = bonus[base + cur]; break; }
-    if (accept[base + main_c]) {
+  while (true) {  // every step moves to a higher row, so at most n1 steps
+    const int main_c = s_main[cur];
+    if (main_c == NONE) { nxt = s_bonus[cur]; break; }
+    if (s_acc[main_c]) {
       path[base + len++] = main_c;
       cur = main_c;
       continue;
     }
-    const int rs = resample[base + main_c];
+    const int rs = s_rs[main_c];
     int sib = -1;
     for (int c = main_c + 1; c < n1; ++c)
-      if (par[base + c] == cur && tok[base + c] == rs) { sib = c; break; }
+      if (s_par[c] == cur && s_tok[c] == rs) { sib = c; break; }
     if (sib < 0) { nxt = rs; break; }
     path[base + len++] = sib;
     cur = sib;
@@ -89,12 +111,13 @@ __global__ void walk_tail_kernel(const uint8_t *__restrict__ accept,
 
 namespace acespec {
 
-hipError_t launch_walk(const int32_t *tok, const int32_t *par, const uint8_t *accept,
+hipError_t launch_walk(const int32_t *tok, const int32_t *par, const int32_t *depth,
+                       const uint8_t *accept,
                        const int32_t *resample, const int32_t *bonus, int B, int n1,
                        int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
                        int32_t *next_token, uint8_t *sibling_hit, hipStream_t s) {
-  if (n1 > MAXN1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(walk_kernel, dim3((B + 63) / 64), dim3(64), 0, s, tok, par, accept,
+  if (n1 > WALK_THREADS) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(walk_kernel, dim3(B), dim3(WALK_THREADS), 0, s, tok, par, depth, accept,
                      resample, bonus, B, n1, acc_prefix_len, path, path_len, next_token,
                      sibling_hit);
   return hipGetLastError();
