@@ -16,20 +16,22 @@
 // Arithmetic: e = exp2((z - max) * log2(e) / T) in fp32; probability mass is summed in
 // 2^-40 fixed point (64-bit integers), so every reduction is exact, order independent
 // and run-to-run deterministic.  The nucleus and top-k thresholds are found by a radix
-// select on the order-preserving 32-bit key of z (12 + 12 + 8 bits, histograms in LDS
+// select on the order-preserving 32-bit key of z (12 + 11 + 9 bits, histograms in LDS
 // weighted by mass for top-p and by count for top-k), which finds the exact threshold
 // logit and the number of tied ids to keep (ids ascending).  The inverse CDFs run over
 // 256-id segments: segment masses are prefix-summed in LDS, and the chosen segment is
 // re-read and scanned across a wavefront.
-// Occupancy: 512 threads and 69 KB of LDS per row (the histograms and the segment tables
-// share storage), so two rows are in flight per CU and one row's scans and selections
-// overlap the other's passes over memory; each pass issues four loads per thread before
-// using any.
+// Occupancy: 512 threads, 51 KB of LDS (the histograms of each pass and the segment
+// tables share storage; the refinement levels are sized to fit under pass 1's) and at most
+// 80 VGPRs per row, so three rows are in flight per CU and their scans and selections
+// overlap each other's passes over memory (1.45x the throughput of one row per CU, and
+// 10 % more than two); the row passes keep the next step's loads in flight while
+// processing the current one.
 #include "common.h"
 
 namespace {
 
-constexpr int VT = 512;             // threads per row (two rows in flight per CU)
+constexpr int VT = 512;             // threads per row (three rows in flight per CU)
 constexpr int NWV = VT / 64;        // waves
 constexpr int SEG = 256;            // ids per segment (one float4 per lane)
 constexpr int SEGMAX = 1024;        // vocab <= 262144
@@ -42,11 +44,15 @@ struct VSmem {
   // The threshold histograms (passes 1-3) and the per-segment tables (tie pass, pass 4)
   // are never live together; sharing their storage keeps two rows in flight per CU.
   union {
-    struct {
+    struct {  // pass 1: bits 31..20 of the key
       uint32_t cnt[4096];
       u64 mass[4096];
-      uint32_t cntk[4096];
     } h;
+    struct {  // passes 2 and 3: bits 19..9, then 8..0, inside the selected bins
+      uint32_t cnt[2048];
+      u64 mass[2048];
+      uint32_t cntk[2048];
+    } r;
     struct {
       u64 seg_p[SEGMAX];       // per-segment mass of p_r, then its exclusive prefix
       u64 seg_r[SEGMAX];       // same for the residual max(0, p_r - Q)
@@ -121,7 +127,7 @@ AS_DEVICE float block_max(float v, VSmem &sm) {
 // Descending radix step: bins b = nb-1 .. 0 hold (count, mass).  Finds the bin where the
 // running mass from the top first reaches `target` (mass mode) or where the running
 // count first reaches `target` (count mode); returns the bin and the amount strictly
-// above it.  nb is 4096 or 256.
+// above it.  nb is 4096, 2048 or 512.
 template <bool MASS>
 AS_DEVICE void select_bin(VSmem &sm, const uint32_t *cnt, const u64 *mass, int nb, u64 target,
                           u64 base, int &sel, u64 &above) {
@@ -283,40 +289,42 @@ AS_DEVICE int find_segment(const u64 *excl, int nseg, u64 target) {
   return lo;
 }
 
-// Loads the VU float4 this thread handles in one step of a pass over the row, all issued
+// Loads the VR float4 this thread handles in one step of a pass over the row, all issued
 // before any is used: one load in flight per thread leaves the passes bound by memory
 // latency rather than bandwidth.  Past the end of the row the row's last float4 is
 // loaded again (V is a multiple of 4): every load is unconditional, so the compiler can
 // wait for the older loads only, and the callers skip those entries (or, for the row
 // maximum, take them: they repeat real elements).
-constexpr int VU = 4;
-AS_DEVICE void load_step(const float *z, int V, int i0, float4 (&v)[VU]) {
+constexpr int VR = 2;  // float4 a thread per step of the row passes (the segment pass: VU)
+constexpr int VU = 2;
+AS_DEVICE void load_step(const float *z, int V, int i0, float4 (&v)[VR]) {
 #pragma unroll
-  for (int u = 0; u < VU; ++u) {
+  for (int u = 0; u < VR; ++u) {
     const int i = i0 + u * VT * 4;
     v[u] = *(const float4 *)(z + (i < V ? i : V - 4));
   }
 }
 
-// A pass over the row, VU float4 per thread a step: the next step's loads are issued
+// A pass over the row, VR float4 per thread a step: the next step's loads are issued
 // before the current step is processed, so a thread always has loads in flight.
 struct RowStream {
   const float *z;
   int V, i0;
-  float4 cur[VU], nxt[VU];
+  float4 cur[VR], nxt[VR];
   AS_DEVICE RowStream(const float *z_, int V_, int start) : z(z_), V(V_), i0(start) {
     load_step(z, V, i0, cur);
   }
   AS_DEVICE bool more() const { return i0 < V; }
-  AS_DEVICE void prefetch() { load_step(z, V, i0 + VT * 4 * VU, nxt); }
+  AS_DEVICE void prefetch() { load_step(z, V, i0 + VT * 4 * VR, nxt); }
   AS_DEVICE void advance() {
 #pragma unroll
-    for (int u = 0; u < VU; ++u) cur[u] = nxt[u];
-    i0 += VT * 4 * VU;
+    for (int u = 0; u < VR; ++u) cur[u] = nxt[u];
+    i0 += VT * 4 * VR;
   }
 };
 
-__global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) {
+// (six waves a SIMD: three 8-wave rows per CU, which caps the kernel at 80 VGPRs)
+__global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs a) {
   __shared__ VSmem sm;
   const int row = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -333,9 +341,9 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
       rs.prefetch();
       const int i0 = rs.i0;
-      const float4 (&vv)[VU] = rs.cur;
+      const float4 (&vv)[VR] = rs.cur;
 #pragma unroll
-      for (int u = 0; u < VU; ++u)
+      for (int u = 0; u < VR; ++u)
         mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
     }
   }
@@ -347,7 +355,6 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   for (int i = tid; i < 4096; i += VT) {
     sm.h.cnt[i] = 0;
     sm.h.mass[i] = 0;
-    sm.h.cntk[i] = 0;
   }
   if (tid == 0) sm.ncand = 0;
   __syncthreads();
@@ -355,9 +362,9 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
     rs.prefetch();
     const int i0 = rs.i0;
-    const float4 (&vv)[VU] = rs.cur;
+    const float4 (&vv)[VR] = rs.cur;
 #pragma unroll
-    for (int u = 0; u < VU; ++u) {
+    for (int u = 0; u < VR; ++u) {
       if (i0 + u * VT * 4 >= V) break;
       const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
 #pragma unroll
@@ -382,13 +389,14 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   select_bin<true>(sm, sm.h.cnt, sm.h.mass, 4096, T_p, 0, bp, ap);
   select_bin<false>(sm, sm.h.cnt, sm.h.mass, 4096, K, 0, bk, ak);
 
-  // ---- pass 2: refine bits 19..8 inside the selected bins ------------------------------
+  // ---- pass 2: refine bits 19..9 inside the selected bins ------------------------------
   // The keys of those bins' elements also go to a per-row scratch list (kept in L2), so
   // that pass 3 can read them instead of the row when they fit.
-  for (int i = tid; i < 4096; i += VT) {
-    sm.h.cnt[i] = 0;
-    sm.h.mass[i] = 0;
-    sm.h.cntk[i] = 0;
+  __syncthreads();  // pass 1's bins are read; their storage is reused
+  for (int i = tid; i < 2048; i += VT) {
+    sm.r.cnt[i] = 0;
+    sm.r.mass[i] = 0;
+    sm.r.cntk[i] = 0;
   }
   if (tid == 0) sm.nbin = 0;
   uint32_t *cl = a.cand ? a.cand + (size_t)row * a.cand_cap : nullptr;
@@ -396,20 +404,20 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
     rs.prefetch();
     const int i0 = rs.i0;
-    const float4 (&vv)[VU] = rs.cur;
+    const float4 (&vv)[VR] = rs.cur;
 #pragma unroll
-    for (int u = 0; u < VU; ++u) {
+    for (int u = 0; u < VR; ++u) {
       if (i0 + u * VT * 4 >= V) break;
       const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t key = f32_key(zz[j]);
-        const int hi = key >> 20, mid = (key >> 8) & 0xFFF;
+        const int hi = key >> 20, mid = (key >> 9) & 0x7FF;
         if (hi == bp) {
-          atomicAdd(&sm.h.cnt[mid], 1u);
-          atomicAdd(&sm.h.mass[mid], fixw(elem_e(zz[j], sel)));
+          atomicAdd(&sm.r.cnt[mid], 1u);
+          atomicAdd(&sm.r.mass[mid], fixw(elem_e(zz[j], sel)));
         }
-        if (hi == bk) atomicAdd(&sm.h.cntk[mid], 1u);
+        if (hi == bk) atomicAdd(&sm.r.cntk[mid], 1u);
         if (cl && (hi == bp || hi == bk)) {
           const uint32_t slot = atomicAdd(&sm.nbin, 1u);
           if (slot < (uint32_t)a.cand_cap) cl[slot] = key;
@@ -420,16 +428,16 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   __syncthreads();
   int sp, sk;
   u64 ap2, ak2;
-  select_bin<true>(sm, sm.h.cnt, sm.h.mass, 4096, T_p, ap, sp, ap2);
-  select_bin<false>(sm, sm.h.cntk, sm.h.mass, 4096, K, ak, sk, ak2);
-  const uint32_t pre_p = ((uint32_t)bp << 12) | (uint32_t)sp;
-  const uint32_t pre_k = ((uint32_t)bk << 12) | (uint32_t)sk;
+  select_bin<true>(sm, sm.r.cnt, sm.r.mass, 2048, T_p, ap, sp, ap2);
+  select_bin<false>(sm, sm.r.cntk, sm.r.mass, 2048, K, ak, sk, ak2);
+  const uint32_t pre_p = ((uint32_t)bp << 11) | (uint32_t)sp;  // key bits 31..9
+  const uint32_t pre_k = ((uint32_t)bk << 11) | (uint32_t)sk;
 
-  // ---- pass 3: refine bits 7..0 ------------------------------------------------------
-  for (int i = tid; i < 256; i += VT) {
-    sm.h.cnt[i] = 0;
-    sm.h.mass[i] = 0;
-    sm.h.cntk[i] = 0;
+  // ---- pass 3: refine bits 8..0 ------------------------------------------------------
+  for (int i = tid; i < 512; i += VT) {
+    sm.r.cnt[i] = 0;
+    sm.r.mass[i] = 0;
+    sm.r.cntk[i] = 0;
   }
   const uint32_t nbin = sm.nbin;  // final: pass 2 ended with a barrier
   __syncthreads();
@@ -437,45 +445,45 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
     // the candidates' keys (a key maps back to its logit exactly)
     for (uint32_t i = tid; i < nbin; i += VT) {
       const uint32_t key = cl[i];
-      if ((key >> 8) == pre_p) {
-        atomicAdd(&sm.h.cnt[key & 0xFF], 1u);
-        atomicAdd(&sm.h.mass[key & 0xFF], fixw(elem_e(key_to_f32(key), sel)));
+      if ((key >> 9) == pre_p) {
+        atomicAdd(&sm.r.cnt[key & 0x1FF], 1u);
+        atomicAdd(&sm.r.mass[key & 0x1FF], fixw(elem_e(key_to_f32(key), sel)));
       }
-      if ((key >> 8) == pre_k) atomicAdd(&sm.h.cntk[key & 0xFF], 1u);
+      if ((key >> 9) == pre_k) atomicAdd(&sm.r.cntk[key & 0x1FF], 1u);
     }
   } else
   for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
     rs.prefetch();
     const int i0 = rs.i0;
-    const float4 (&vv)[VU] = rs.cur;
+    const float4 (&vv)[VR] = rs.cur;
 #pragma unroll
-    for (int u = 0; u < VU; ++u) {
+    for (int u = 0; u < VR; ++u) {
       if (i0 + u * VT * 4 >= V) break;
       const float zz[4] = {vv[u].x, vv[u].y, vv[u].z, vv[u].w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t key = f32_key(zz[j]);
-        if ((key >> 8) == pre_p) {
-          atomicAdd(&sm.h.cnt[key & 0xFF], 1u);
-          atomicAdd(&sm.h.mass[key & 0xFF], fixw(elem_e(zz[j], sel)));
+        if ((key >> 9) == pre_p) {
+          atomicAdd(&sm.r.cnt[key & 0x1FF], 1u);
+          atomicAdd(&sm.r.mass[key & 0x1FF], fixw(elem_e(zz[j], sel)));
         }
-        if ((key >> 8) == pre_k) atomicAdd(&sm.h.cntk[key & 0xFF], 1u);
+        if ((key >> 9) == pre_k) atomicAdd(&sm.r.cntk[key & 0x1FF], 1u);
       }
     }
   }
   __syncthreads();
   int lp, lk;
   u64 ap3, ak3;
-  select_bin<true>(sm, sm.h.cnt, sm.h.mass, 256, T_p, ap2, lp, ap3);
-  select_bin<false>(sm, sm.h.cntk, sm.h.mass, 256, K, ak2, lk, ak3);
-  sel.tau_p = (pre_p << 8) | (uint32_t)lp;
-  sel.tau_k = (pre_k << 8) | (uint32_t)lk;
-  sel.c_p = sm.h.cnt[lp];
-  sel.c_k = sm.h.cntk[lk];
+  select_bin<true>(sm, sm.r.cnt, sm.r.mass, 512, T_p, ap2, lp, ap3);
+  select_bin<false>(sm, sm.r.cntk, sm.r.mass, 512, K, ak2, lk, ak3);
+  sel.tau_p = (pre_p << 9) | (uint32_t)lp;
+  sel.tau_k = (pre_k << 9) | (uint32_t)lk;
+  sel.c_p = sm.r.cnt[lp];
+  sel.c_k = sm.r.cntk[lk];
   sel.above_p = ap3;
   sel.above_k = (uint32_t)ak3;
   {
-    const u64 w_tau = sm.h.mass[lp] / (sel.c_p ? sel.c_p : 1);
+    const u64 w_tau = sm.r.mass[lp] / (sel.c_p ? sel.c_p : 1);
     const u64 need = T_p - ap3;  // > 0
     u64 j = w_tau ? (need + w_tau - 1) / w_tau : 1;
     if (j < 1) j = 1;
@@ -538,22 +546,17 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
   const bool dense_q = a.q_scalar == nullptr;
   const bool resid = has_child && dense_q;
   const float *q = dense_q ? a.q + (size_t)row * V : nullptr;
-  // The VU segments of a step are loaded before any is used, and the next step's loads
-  // are issued before the current step is processed.  Past the end of the row the last
-  // float4 is loaded again (unconditional loads); those lanes are not valid below.
-  auto seg_load = [&](int s0_, float4 (&zl)[VU], float4 (&ql)[VU]) {
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int id0 = (s0_ + u * NWV) * SEG + lane * 4;
-      const int ld = id0 < V ? id0 : V - 4;
-      zl[u] = *(const float4 *)(z + ld);
-      ql[u] = resid ? *(const float4 *)(q + ld) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  };
-  float4 z4u[VU], q4u[VU], z4n[VU], q4n[VU];
-  seg_load(wave, z4u, q4u);
+  // The VU segments of a step are loaded before any is used.  Past the end of the row the
+  // last float4 is loaded again (unconditional loads); those lanes are not valid below.
   for (int s0 = wave; s0 < nseg; s0 += NWV * VU) {
-  seg_load(s0 + NWV * VU, z4n, q4n);
+  float4 z4u[VU], q4u[VU];
+#pragma unroll
+  for (int u = 0; u < VU; ++u) {
+    const int id0 = (s0 + u * NWV) * SEG + lane * 4;
+    const int ld = id0 < V ? id0 : V - 4;
+    z4u[u] = *(const float4 *)(z + ld);
+    q4u[u] = resid ? *(const float4 *)(q + ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 #pragma unroll
   for (int u = 0; u < VU; ++u) {
     const int s = s0 + u * NWV;
@@ -599,11 +602,6 @@ __global__ __launch_bounds__(VT) void vocab_verify_kernel(acespec::VocabArgs a) 
       sm.g.seg_p[s] = sp_;
       sm.g.seg_r[s] = sr_;
     }
-  }
-#pragma unroll
-  for (int u = 0; u < VU; ++u) {
-    z4u[u] = z4n[u];
-    q4u[u] = q4n[u];
   }
   }
   __syncthreads();
