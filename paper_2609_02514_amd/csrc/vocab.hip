@@ -24,9 +24,9 @@
 // Occupancy: 512 threads, 51 KB of LDS (the histograms of each pass and the segment
 // tables share storage; the refinement levels are sized to fit under pass 1's) and at most
 // 80 VGPRs per row, so three rows are in flight per CU and their scans and selections
-// overlap each other's passes over memory (1.45x the throughput of one row per CU, and
-// 10 % more than two); the row passes keep the next step's loads in flight while
-// processing the current one.
+// overlap each other's passes over memory (two rows a CU give about 1.45x the throughput
+// of one, three about 10 % more than two); the row passes keep the next step's loads in
+// flight while processing the current one.
 #include "common.h"
 
 namespace {
