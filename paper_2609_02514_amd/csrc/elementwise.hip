@@ -14,15 +14,6 @@
 
 namespace {
 
-template <typename T>
-__global__ void embed_kernel(const T *__restrict__ embed, const int32_t *__restrict__ tok,
-                             float *__restrict__ x, int d) {
-  const int row = blockIdx.x;
-  const T *src = embed + (size_t)tok[row] * d;
-  float *dst = x + (size_t)row * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = to_f32(src[i]);
-}
-
 // Four consecutive elements as float4 (the row bases are 16-byte aligned: d % 64 == 0).
 AS_DEVICE float4 load4(const float *p, int c) { return *(const float4 *)(p + 4 * c); }
 AS_DEVICE float4 load4(const bf16 *p, int c) {
@@ -34,6 +25,16 @@ AS_DEVICE void store4(float *p, int c, float4 v) { *(float4 *)(p + 4 * c) = v; }
 AS_DEVICE void store4(f16 *p, int c, float4 v) {
   typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
   *(f16x4 *)(p + 4 * c) = f16x4{(f16)v.x, (f16)v.y, (f16)v.z, (f16)v.w};
+}
+
+// One row per block, four elements a thread per step (d % 64 == 0).
+template <typename T>
+__global__ void embed_kernel(const T *__restrict__ embed, const int32_t *__restrict__ tok,
+                             float *__restrict__ x, int d) {
+  const int row = blockIdx.x;
+  const T *src = embed + (size_t)tok[row] * d;
+  float *dst = x + (size_t)row * d;
+  for (int c = threadIdx.x; c < (d >> 2); c += blockDim.x) store4(dst, c, load4(src, c));
 }
 
 // One 256-thread block per row; d is a multiple of 64.  A row of up to 8192 values is read
