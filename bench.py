@@ -144,17 +144,49 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_mib
     return out
 
 
-def load_traffic(workload):
-    """Measured HBM bytes per launch per kernel kind from the committed counter summary,
-    or {} -- a kind whose sources changed since the counters were taken is dropped."""
-    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+def summarize_mfma(run_dir):
+    """Per-kind MFMA pipe utilisation from one rocprofv3 pass of rocprofiler's derived
+    counter MfmaUtil (SQ_VALU_MFMA_BUSY_CYCLES summed over the SIMDs / (GRBM_GUI_ACTIVE x
+    SIMDs), in percent per dispatch): the hardware's view of how busy the matrix cores are,
+    independent of the clock the power limit sets."""
+    rows = [r for r in _pmc_rows(run_dir) if r.get("Counter_Name", "MfmaUtil") == "MfmaUtil"]
+    acc = {}
+    for kind, r in zip(_label_dispatches(rows), rows):
+        if kind is None or kind == "+":
+            continue
+        acc.setdefault(kind, []).append(float(r["Counter_Value"]))
+    return {"counter": "MfmaUtil", "kinds": {
+        k: {"launches": len(v), "mfma_busy_pct": round(sum(v) / len(v), 2),
+            "source_sha": kind_source_hash(k)} for k, v in sorted(acc.items())}}
+
+
+def _profile_blob(name):
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
-        return {}
+        return None
     text = open(path).read()
     i = text.find("```json")
     if i < 0:
+        return None
+    return json.loads(text[i + 7: text.index("```", i + 7)])
+
+
+def load_mfma(workload):
+    """Measured MFMA busy percentage per kernel kind from the committed counter summary, or
+    {} -- a kind whose sources changed since the counters were taken is dropped."""
+    blob = _profile_blob(f"mfma_util_{workload}.md")
+    if blob is None:
         return {}
-    blob = json.loads(text[i + 7: text.index("```", i + 7)])
+    return {k: v["mfma_busy_pct"] for k, v in blob["kinds"].items()
+            if v.get("source_sha") == kind_source_hash(k)}
+
+
+def load_traffic(workload):
+    """Measured HBM bytes per launch per kernel kind from the committed counter summary,
+    or {} -- a kind whose sources changed since the counters were taken is dropped."""
+    blob = _profile_blob(f"hbm_traffic_{workload}.md")
+    if blob is None:
+        return {}
     return {k: v["hbm_bytes_per_launch"] for k, v in blob["kinds"].items()
             if v.get("source_sha") == kind_source_hash(k)}
 
@@ -242,9 +274,15 @@ def main():
                          "output directories (bench FETCH_SIZE, bench WRITE_SIZE, copy "
                          "FETCH_SIZE, copy WRITE_SIZE)")
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="print the per-kernel MFMA busy summary of one rocprofv3 "
+                         "--pmc MfmaUtil output directory")
     args = ap.parse_args()
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.copy_mib), indent=1))
+        return
+    if args.summarize_mfma:
+        print(json.dumps(summarize_mfma(args.summarize_mfma), indent=1))
         return
     if args.copy_calibration:
         import torch
@@ -362,9 +400,12 @@ def main():
         f"{value:.0f} tok/s; status {outs['status'].tolist()[:4]}...")
 
     traffic = load_traffic(w.name)
+    mfma_busy = load_mfma(w.name)
     for name, ent in kernels.items():
         if name in traffic:
             ent["hbm_traffic_bytes_per_launch"] = traffic[name]
+        if name in mfma_busy:
+            ent["mfma_busy_pct_pmc"] = mfma_busy[name]
     if dom.startswith("gemm"):
         roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dk["mfma_frac"],

@@ -140,3 +140,28 @@ def test_committed_traffic_tables_name_known_kernels():
         assert set(blob["kinds"]) <= set(bench.KIND_SOURCES)
         for v in blob["kinds"].values():
             assert v["hbm_bytes_per_launch"] > 0 and len(v["source_sha"]) == 16
+
+
+def test_mfma_summary_averages_per_kind_and_skips_fixups(tmp_path, monkeypatch):
+    # one MfmaUtil value per dispatch (percent), in dispatch order
+    util = {i: 5.0 * (i + 1) for i in range(len(_STEP))}
+    rows = [{"Dispatch_Id": str(i), "Kernel_Name": _STEP[i][0], "Counter_Value": str(util[i])}
+            for i in reversed(range(len(_STEP)))]
+    _write_counters(str(tmp_path / "m"), rows)
+    out = bench.summarize_mfma(str(tmp_path / "m"))
+    k = out["kinds"]
+    assert k["gemm_qkv"] == {"launches": 2, "mfma_busy_pct": round((util[1] + util[11]) / 2, 2),
+                             "source_sha": bench.kind_source_hash("gemm_qkv")}
+    assert k["gemm_o"]["mfma_busy_pct"] == util[5]          # its fixup is not averaged in
+    assert k["gemm_gate_up"]["mfma_busy_pct"] == util[7]
+    assert "+" not in k and None not in k
+    # committed summaries are read back only for kinds whose sources are unchanged
+    blob = {"counter": "MfmaUtil", "kinds": {
+        "gemm_o": {"launches": 1, "mfma_busy_pct": 41.5, "source_sha": bench.kind_source_hash("gemm_o")},
+        "tree_attention": {"launches": 1, "mfma_busy_pct": 9.0, "source_sha": "0000000000000000"}}}
+    os.makedirs(tmp_path / "profiles")
+    (tmp_path / "profiles" / "mfma_util_x.md").write_text(
+        "# table\n\n```json\n" + json.dumps(blob) + "\n```\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.load_mfma("x") == {"gemm_o": 41.5}
+    assert bench.load_mfma("missing") == {}
