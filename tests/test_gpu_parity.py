@@ -1,6 +1,8 @@
 """GPU parity: the HIP path (through the C ABI) against the float64 oracle on the same
 seeded inputs.  Logits are compared element by element; decisions are compared with the
 oracle's verify stage run on the GPU's own logits, every mismatch classified."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -118,7 +120,7 @@ def test_tree_paper_scale_widths(name):
 # ---------------------------------------------------------------------------------------
 
 
-def _run_tail(w, W=None, rows_check=None, tol=1e-4):
+def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False):
     from paper_2609_02514_amd.acespec import Verifier
     dev = "cuda"
     W = W or synth.make_weights(w, dev)
@@ -128,13 +130,13 @@ def _run_tail(w, W=None, rows_check=None, tol=1e-4):
     v = Verifier.for_workload(w)
     outs = v.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, dev, True)
     hz.log(f"verify_tail R={R} V={w.V}")
-    v.verify_tail(W.lm_head, None, batch.hidden, batch.draft_tokens, batch.q, batch.u,
-                  w.chain_len, w.T, w.top_p, w.top_k, outs)
+    v.verify_tail(W.lm_head, W.final_norm if final_norm else None, batch.hidden,
+                  batch.draft_tokens, batch.q, batch.u, w.chain_len, w.T, w.top_p, w.top_k, outs)
     torch.cuda.synchronize()
     g = {k: (hz.host(t) if t is not None else None) for k, t in outs.items()}
     v.close()
     rows = list(range(R)) if rows_check is None else rows_check
-    z_ref = om.lm_head_tail(W, batch.hidden[rows])
+    z_ref = om.lm_head_tail(W, batch.hidden[rows], final_norm=final_norm, eps=w.rms_eps)
     zg = g["logits_out"][rows].numpy().astype(np.float64)
     err = hz.logits_rel_err(zg, z_ref)
     hz.log(f"tail logits max rel err {err.max():.3e}")
@@ -162,6 +164,17 @@ def test_tail_small():
     w = synth.get("8b-lmhead-tail").scaled(name="tail-small", d=256, V=5004, rows=96,
                                           chain_len=8, top_k=16)
     _run_tail(w)
+
+
+def test_tail_with_final_norm():
+    """A non-NULL final_norm: the tail rows are RMS-normalised with the gain (rounded to
+    fp16 for the LM head) before the product; the oracle normalises in float64."""
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-norm", d=256, V=5004, rows=64,
+                                          chain_len=8, top_k=16)
+    W = synth.make_weights(w, "cuda")
+    gain = 1.0 + synth.normal((w.d,), 0.1, torch.float32, "cuda", w.seed_base, 0, 2)
+    W = dataclasses.replace(W, final_norm=gain.to(torch.bfloat16))
+    _run_tail(w, W=W, tol=2e-3, final_norm=True)
 
 
 def test_tail_exact_logit_ties():
