@@ -177,6 +177,16 @@ def test_tail_with_final_norm():
     _run_tail(w, W=W, tol=2e-3, final_norm=True)
 
 
+def test_tail_fp32_model_with_final_norm():
+    """The fp32 model's tail (reference-precision kernels) with a final RMSNorm gain."""
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-f32", dtype="f32", d=192, V=3000,
+                                          rows=48, chain_len=6, top_k=24)
+    W = synth.make_weights(w, "cuda")
+    gain = 1.0 + synth.normal((w.d,), 0.1, torch.float32, "cuda", w.seed_base, 0, 2)
+    W = dataclasses.replace(W, final_norm=gain)
+    _run_tail(w, W=W, tol=1e-4, final_norm=True)
+
+
 def test_tail_exact_logit_ties():
     """Duplicated LM-head rows give exactly equal logits: ties must be broken by token id
     in the nucleus, the top-k payload and the inverse CDFs."""
