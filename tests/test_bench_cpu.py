@@ -165,3 +165,15 @@ def test_mfma_summary_averages_per_kind_and_skips_fixups(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     assert bench.load_mfma("x") == {"gemm_o": 41.5}
     assert bench.load_mfma("missing") == {}
+
+
+def test_committed_mfma_tables_name_known_kernels():
+    d = os.path.join(bench.ROOT, "profiles")
+    tables = [f for f in os.listdir(d) if f.startswith("mfma_util_") and f.endswith(".md")]
+    assert tables
+    for f in tables:
+        blob = bench._profile_blob(f)
+        assert blob["counter"] == "MfmaUtil"
+        assert set(blob["kinds"]) <= set(bench.KIND_SOURCES)
+        for v in blob["kinds"].values():
+            assert 0.0 <= v["mfma_busy_pct"] <= 100.0 and len(v["source_sha"]) == 16
