@@ -191,18 +191,46 @@ def load_traffic(workload):
             if v.get("source_sha") == kind_source_hash(k)}
 
 
-def cpu_baseline(w, W, batch, n_sessions):
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _threads_in_use():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def one_thread(fn, *a):
+    """fn(*a) with numpy's BLAS and torch's intra-op pool limited to one thread."""
+    import torch
+    from threadpoolctl import threadpool_limits
+    nt = torch.get_num_threads()
+    torch.set_num_threads(1)
+    try:
+        with threadpool_limits(1):
+            return fn(*a)
+    finally:
+        torch.set_num_threads(nt)
+
+
+def cpu_baseline(w, W, batch, n_sessions, sessions=None):
     """The oracle as it stands on n_sessions whole sessions: the tree forward through every
     layer, the verify stage of every row and the walk."""
     import numpy as np
     from oracle import model as om
     from oracle import verify as ov
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        cores = os.cpu_count() or 1
-    sess = list(range(min(n_sessions, batch.tokens.shape[0])))
+    cores = _threads_in_use()
+    sess = (list(sessions) if sessions is not None
+            else list(range(min(n_sessions, batch.tokens.shape[0]))))
     # host copies of everything the sample reads, taken before the oracle clock starts
     Wh = type(W)(W.embed.cpu(), [{k: v.cpu() for k, v in lw.items()} for lw in W.layers],
                  W.final_norm.cpu(), W.lm_head.cpu())
@@ -210,8 +238,8 @@ def cpu_baseline(w, W, batch, n_sessions):
     kv = {(l, b): (om.k_prefix(batch.kv_k, l, b, S[b]), om.v_prefix(batch.kv_v, l, b, S[b]))
           for l in range(w.L) for b in sess}
     toks, pars = batch.tokens.cpu(), batch.parents.cpu()
-    q = batch.q[: len(sess)].cpu().numpy().astype(np.float64)
-    u = batch.u[: len(sess)].cpu().numpy().astype(np.float64)
+    q = batch.q[sess].cpu().numpy().astype(np.float64)
+    u = batch.u[sess].cpu().numpy().astype(np.float64)
     t0 = time.perf_counter()
     z = om.forward_tree_batch(Wh, om.dims_of(w), toks, pars, batch.prefix_len.cpu(),
                               lambda l, b: kv[(l, b)], sess)
@@ -222,9 +250,13 @@ def cpu_baseline(w, W, batch, n_sessions):
         ov.walk(tk, pr, res)
     t = time.perf_counter() - t0
     n_tok = len(sess) * (toks.shape[1] - 1)
+    B = batch.tokens.shape[0]
     return {"value": n_tok / t, "unit": "verified tree tokens/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": (f"{len(sess)} of {batch.tokens.shape[0]} sessions of {w.name} "
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "extrapolated": (f"linear in sessions (each session's outputs depend on its own "
+                             f"inputs only): {len(sess)} of {B} sessions timed")
+            if len(sess) < B else None,
+            "sample": (f"{len(sess)} of {B} sessions of {w.name} "
                        f"({n_tok} drafted nodes): full float64 forward through all {w.L} "
                        f"layers, verify stage of every row, walk; {t:.1f} s")}
 
@@ -235,11 +267,7 @@ def cpu_baseline_tail(w, W, batch, n_chains):
     import numpy as np
     from oracle import model as om
     from oracle import verify as ov
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    except Exception:
-        cores = os.cpu_count() or 1
+    cores = _threads_in_use()
     rows = list(range(min(n_chains * w.chain_len, w.rows)))
     Wh = type(W)(None, [], None, W.lm_head.cpu())
     hid = batch.hidden[rows].cpu()
@@ -252,10 +280,65 @@ def cpu_baseline_tail(w, W, batch, n_chains):
     ov.walk_tail(res["accept"], res["resample"], w.chain_len)
     t = time.perf_counter() - t0
     return {"value": len(rows) / t, "unit": "verified tree tokens/s", "cores": int(cores),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "extrapolated": (f"linear in rows (each row's outputs depend on its own inputs "
+                             f"only): {len(rows)} of {w.rows} rows timed")
+            if len(rows) < w.rows else None,
             "sample": (f"{len(rows) // w.chain_len} of {w.rows // w.chain_len} chains of {w.name} "
                        f"({len(rows)} rows): float64 LM head, verify stage of every row, chain "
                        f"walk; {t:.1f} s")}
+
+
+# ---------------------------------------------------------------------------------------
+# Achievable peaks: what this chip sustains, measured beside the published figures
+# ---------------------------------------------------------------------------------------
+
+
+def calibrate(reps=5):
+    """Median rate of (a) a plain 1 GiB device copy and (b) the MFMA pipe on random fp16
+    operands (v_mfma_f32_16x16x32_f16, 16 independent accumulators a wave, no memory
+    traffic in the loop), both timed with HIP events on the current stream."""
+    import ctypes
+    import statistics
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02514_amd", "libacespec_calib.so"))
+    lib.acespec_calib_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_int, ctypes.c_void_p]
+    lib.acespec_calib_mfma.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                       ctypes.c_int, ctypes.c_void_p]
+    stream = torch.cuda.current_stream()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    blocks, iters = 3 * cus, 20000      # 3 waves a SIMD (the kernel's occupancy limit)
+    ops = torch.randn(blocks * 256 * 64, device="cuda").to(torch.float16)
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        ts = []
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            assert rc == 0, rc
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts[1:])   # the first run warms up
+
+    ms_copy = timed(lambda: lib.acespec_calib_copy(src.data_ptr(), dst.data_ptr(), nbytes,
+                                                   cus * 16, stream.cuda_stream))
+    ms_mfma = timed(lambda: lib.acespec_calib_mfma(ops.data_ptr(), out.data_ptr(), blocks,
+                                                   iters, stream.cuda_stream))
+    flops = blocks * 4 * iters * 16 * 16384.0
+    del src, dst, ops, out
+    return {"hbm_copy_gbs": round(2 * nbytes / (ms_copy / 1e3) / 1e9, 1),
+            "mfma_f16_loop_tflops": round(flops / (ms_mfma / 1e3) / 1e12, 1),
+            "method": (f"median of {reps} HIP-event-timed runs: a 1 GiB device copy "
+                       f"(16-byte loads and stores, read + write bytes counted), and "
+                       f"{blocks} workgroups x 4 waves x {iters} x 16 MFMAs 16x16x32 f16 on "
+                       f"random operands")}
 
 
 def main():
@@ -265,7 +348,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b-bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sessions", type=int, default=3)
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step into a HIP graph (stream capture) and time its "
+                         "replays; the dominant kernel's launches are then timed in as many "
+                         "eager steps run right after the timed replays")
+    ap.add_argument("--cpu-sessions", type=int, default=4)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run one plain device-to-device copy of MIB MiB (the reference "
                          "kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -359,6 +446,25 @@ def main():
             kernels[name] = ent
         return kernels
 
+    graph = None
+    if args.graph:
+        # The step enqueues kernel launches only (no allocation, memset, synchronisation
+        # or, with timing off, events), so it captures as it is.
+        acespec_timing_enable(v.ctx, False)
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        log("captured one step into a graph")
+
     # Per-kernel breakdown: the same steps with HIP events around every kernel (each
     # recorded pair costs stream time, so this pass is kept out of the timed region).
     acespec_timing_only(v.ctx, None)
@@ -370,34 +476,62 @@ def main():
     kernels = breakdown(acespec_timing_read(v.ctx), args.steps)
     dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
 
-    # Timed region: events only around the dominant kernel kind, and only in a sample of
-    # about five of the timed steps spread over the region (each recorded pair costs
-    # stream time: events around all 32 gate/up launches of every step add ~0.9 % to the
-    # step); their launches give the roofline's average duration, measured live on the
-    # launch stream.
+    # Timed region: exactly K steps, each bracketed by its own HIP event pair on the launch
+    # stream, with the L2 and MALL flushed before every step outside its events (a 512 MB
+    # buffer is read and written: 2x the 256 MB MALL), so no step finds the previous one's
+    # weights or KV in cache; ms/step is the median.  The library records events around
+    # the dominant kernel kind only, and only in about five of the steps (each recorded
+    # pair costs stream time); their launches give the roofline's average duration,
+    # measured live on the launch stream.
+    import statistics
     acespec_timing_only(v.ctx, dom)
     acespec_timing_read(v.ctx)
     every = max(1, args.steps // 5)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flush = torch.zeros((512 << 20) // 4, dtype=torch.float32, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
-    e0.record(stream)
     t_wall = time.perf_counter()
-    for i in range(args.steps):
-        acespec_timing_enable(v.ctx, i % every == 0)
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_total = e0.elapsed_time(e1)
+    if args.graph:
+        acespec_timing_enable(v.ctx, False)
+        for i in range(args.steps):
+            flush.add_(1.0)
+            ev[i][0].record(stream)
+            graph.replay()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+        for i in range(0, args.steps, every):   # the dominant kind, in eager steps
+            flush.add_(1.0)
+            acespec_timing_enable(v.ctx, True)
+            step()
+        acespec_timing_enable(v.ctx, False)
+        torch.cuda.synchronize()
+    else:
+        for i in range(args.steps):
+            flush.add_(1.0)
+            acespec_timing_enable(v.ctx, i % every == 0)
+            ev[i][0].record(stream)
+            step()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        t_wall = time.perf_counter() - t_wall
+    step_ms = [a.elapsed_time(b) for a, b in ev]
     timed_steps = len(range(0, args.steps, every))
     dk = breakdown(acespec_timing_read(v.ctx), timed_steps)[dom]
     acespec_timing_enable(v.ctx, False)
     acespec_timing_only(v.ctx, None)
-    ms_step = ms_total / args.steps
+    del flush
+    ms_step = statistics.median(step_ms)
     tokens = B * n1 if tail else B * (n1 - 1)   # drafted tokens verified per step
     value = tokens / (ms_step / 1e3)
-    log(f"{args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f}), "
-        f"{value:.0f} tok/s; status {outs['status'].tolist()[:4]}...")
+    log(f"{args.steps} steps: median {ms_step:.3f} ms/step (mean {statistics.mean(step_ms):.3f}, "
+        f"min {min(step_ms):.3f}, max {max(step_ms):.3f}; wall incl. flushes "
+        f"{t_wall / args.steps * 1e3:.3f}), {value:.0f} tok/s; "
+        f"status {outs['status'].tolist()[:4]}...")
+    ach = calibrate()
+    log(f"achievable: copy {ach['hbm_copy_gbs']} GB/s, MFMA loop {ach['mfma_f16_loop_tflops']} "
+        f"TFLOP/s")
 
     traffic = load_traffic(w.name)
     mfma_busy = load_mfma(w.name)
@@ -406,13 +540,21 @@ def main():
             ent["hbm_traffic_bytes_per_launch"] = traffic[name]
         if name in mfma_busy:
             ent["mfma_busy_pct_pmc"] = mfma_busy[name]
+    for name, ent in kernels.items():
+        if "tflops" in ent:
+            ent["mfma_frac_achievable"] = round(ent["tflops"] / ach["mfma_f16_loop_tflops"], 4)
+        if "gbs" in ent:
+            ent["hbm_frac_achievable"] = round(ent["gbs"] / ach["hbm_copy_gbs"], 4)
     if dom.startswith("gemm"):
         roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dk["mfma_frac"],
-                "traffic": traffic.get(dom)}
+                "traffic": traffic.get(dom), "achievable": ach["mfma_f16_loop_tflops"],
+                "frac_of_achievable": round(dk["tflops"] / ach["mfma_f16_loop_tflops"], 4)}
     else:
         roof = {"kernel": dom, "bound": "hbm", "achieved": dk["gbs"], "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": dk["hbm_frac"], "traffic": traffic.get(dom)}
+                "unit": "GB/s", "frac": dk["hbm_frac"], "traffic": traffic.get(dom),
+                "achievable": ach["hbm_copy_gbs"],
+                "frac_of_achievable": round(dk["gbs"] / ach["hbm_copy_gbs"], 4)}
     roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["algorithmic_per_launch"] = {"flops": work[dom][0], "bytes": work[dom][1]} if dom in work else None
 
@@ -441,6 +583,11 @@ def main():
         cpu = (cpu_baseline_tail(w, W, batch, args.cpu_sessions * 32) if tail
                else cpu_baseline(w, W, batch, args.cpu_sessions))
         log(f"oracle: {cpu['value']:.3f} tok/s on {cpu['cores']} threads")
+        # per core: one thread on one session (one chain of the tail)
+        one = one_thread(cpu_baseline_tail, w, W, batch, 1) if tail else \
+            one_thread(cpu_baseline, w, W, batch, 1, [min(args.cpu_sessions, B - 1)])
+        cpu["per_core"] = {"value": one["value"], "threads": 1, "sample": one["sample"]}
+        log(f"oracle, one thread: {one['value']:.3f} tok/s")
 
     line = {
         "metric": ("verified tree tokens/s on 1 MI355X (8B shape)" if w.name == "8b-bf16"
@@ -451,6 +598,12 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "step_ms_stats": {"median": round(ms_step, 4), "mean": round(statistics.mean(step_ms), 4),
+                          "min": round(min(step_ms), 4), "max": round(max(step_ms), 4),
+                          "timing": "one HIP event pair per step on the launch stream; L2 and "
+                                    "MALL flushed (512 MB touched) before each step, outside "
+                                    "its events" + ("; each step a replay of one captured "
+                                                    "HIP graph" if args.graph else "")},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -470,6 +623,7 @@ def main():
                           "(the timed region records events around the roofline kernel only, "
                           "in about five of its steps)",
         "commit_kv": commit,
+        "achievable_peaks": ach,
     }
     print(json.dumps(line), flush=True)
     v.close()

@@ -19,10 +19,20 @@
  *    outputs are valid once the stream has completed.
  *  - Argument and shape errors are reported synchronously, before anything is
  *    launched, by a negative return code; acespec_last_error() then holds a message.
- *  - Malformed per-session data found on the device (a parent index that is not an
- *    earlier row, a token id outside the vocabulary, a prefix length that does not fit
- *    the cache) sets status[b] = ACESPEC_EBADTREE for that session only; its other
- *    outputs are then unspecified but every access stays in bounds.
+ *  - Malformed per-session data found on the device sets status[b] for that session
+ *    only; its other outputs are then unspecified but every access stays in bounds:
+ *      ACESPEC_EBADTREE    a parent index that is not an earlier row, a token id outside
+ *                          the vocabulary, a prefix length that does not fit the cache;
+ *      ACESPEC_EBADDRAFT   a draft distribution the step reads holds a NaN, infinite or
+ *                          negative entry (dense draft_q rows with children), or a scalar
+ *                          q_hat outside [0, 1];
+ *      ACESPEC_ENONFINITE  a target logit of the session is not finite: an activation
+ *                          left the range of the 16-bit type it is handed on in (fp16
+ *                          between the kernels of a bf16 model, max 65504), or the
+ *                          weights, KV cache or hidden states hold NaN/inf.
+ *    When several apply the first in this list that the step detects is reported
+ *    (tree checks run before the forward pass; of the two data errors the
+ *    non-finite logits win).
  *  - No C++ exception crosses this interface.
  *  - A context must not be used by two calls that overlap in time (its workspace is
  *    shared by all calls on it).
@@ -43,7 +53,9 @@ typedef enum {
   ACESPEC_EUNSUPPORTED = -2,  /* valid but not supported by these kernels            */
   ACESPEC_ENOMEM = -3,        /* workspace allocation failed in acespec_create        */
   ACESPEC_EHIP = -4,          /* a HIP runtime call failed                            */
-  ACESPEC_EBADTREE = -5       /* per-session status only: malformed tree or prefix    */
+  ACESPEC_EBADTREE = -5,      /* per-session status only: malformed tree or prefix    */
+  ACESPEC_EBADDRAFT = -6,     /* per-session status only: NaN/inf/negative draft data  */
+  ACESPEC_ENONFINITE = -7     /* per-session status only: non-finite target logits     */
 } acespec_status;
 
 typedef enum { ACESPEC_F32 = 0, ACESPEC_BF16 = 1 } acespec_dtype;
@@ -113,7 +125,7 @@ typedef struct {
   int32_t *path_len;        /* [B] drafted tokens kept                                */
   int32_t *next_token;      /* [B] token emitted after the kept path                  */
   uint8_t *sibling_hit;     /* [B] 1 if the walk continued through a drafted sibling */
-  int32_t *status;          /* [B] ACESPEC_OK or ACESPEC_EBADTREE                     */
+  int32_t *status;          /* [B] ACESPEC_OK, or EBADTREE / EBADDRAFT / ENONFINITE   */
   float   *logits_out;      /* optional [rows, vocab] fp32 logits; NULL = not kept    */
 } acespec_outputs;
 
@@ -172,8 +184,10 @@ int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *weight
  * within its chain, counting the row).  Per chain c: path_len[c] = leading accepts,
  * path[c, 0..chain_len) = kept row indices within the chain (-1 padded),
  * next_token[c] = resample at the first rejected row, or -1 when the whole chain is
- * accepted (the bonus then needs the row after the chain); sibling_hit[c] = 0,
- * status[c] = OK.  path is [R/chain_len, chain_len]. */
+ * accepted (the bonus then needs the row after the chain); sibling_hit[c] = 0;
+ * status[c] = OK, EBADTREE (a draft token outside the vocabulary), or EBADDRAFT /
+ * ENONFINITE for a row of the chain (without final_norm, hidden values beyond the fp16
+ * range of a bf16 model overflow and give ENONFINITE).  path is [R/chain_len, chain_len]. */
 int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
                         const void *hidden, const int32_t *draft_tokens,
                         const float *draft_q, const float *uniforms, int R, int chain_len,
@@ -193,7 +207,10 @@ int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final
  * new end keep stale entries.
  *  new_prefix_len [B] DEVICE output: prefix_len[b] + 1 + path_len[b], or -1 for a session
  *  that was not committed (bad status, prefix_len + N + 1 > capacity, path_len outside
- *  [0, N] or a kept row outside [1, N]); nothing of such a session is moved.
+ *  [0, N] or a kept row outside [1, N]); nothing of such a session is moved.  It must not
+ *  overlap kv->prefix_len (every workgroup of a session reads prefix_len[b] while one of
+ *  them writes new_prefix_len[b]): an overlapping pair returns ACESPEC_EINVAL before
+ *  anything is launched.  Copy new_prefix_len into prefix_len after the call instead.
  * The next round's root is the verify step's next_token (not yet in the cache). */
 int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_t *path,
                       const int32_t *path_len, const int32_t *status, int B, int N,

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libacespec.so")
 
 ACESPEC_OK, ACESPEC_EINVAL, ACESPEC_EUNSUPPORTED = 0, -1, -2
 ACESPEC_ENOMEM, ACESPEC_EHIP, ACESPEC_EBADTREE = -3, -4, -5
+ACESPEC_EBADDRAFT, ACESPEC_ENONFINITE = -6, -7
 ACESPEC_F32, ACESPEC_BF16 = 0, 1
 
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",

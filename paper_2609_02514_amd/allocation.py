@@ -1,4 +1,4 @@
-"""Edge-side tree shape of the paper (Section IV): the network-aware budget (Eq. 10) and
+"""Edge-side tree shape of the paper (Section IV): the network-aware budget (Eq. 5) and
 the geometric-decay branch allocation (Eq. 14), in integers.
 
 The optimum of the weighted log hit-rate under the budget puts F*_k = B_alloc (1 - eta) /

@@ -1,4 +1,5 @@
-"""Builds libacespec.so (all HIP sources for gfx950) next to this file.
+"""Builds libacespec.so (all HIP sources of csrc/ for gfx950) next to this file, and
+libacespec_calib.so (calib/: the measurement harness's copy and MFMA-rate kernels).
 
     python -m paper_2609_02514_amd.build
 """
@@ -13,6 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OBJ = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(HERE, "libacespec.so")
+CALIB_SRC = os.path.join(HERE, "calib", "peak.hip")
+CALIB_LIB = os.path.join(HERE, "libacespec_calib.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -52,6 +55,14 @@ def build(verbose=True):
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")
+    tmp = CALIB_LIB + ".tmp"
+    cmd = [HIPCC] + FLAGS + ["-shared", CALIB_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("calibration library build failed:\n" + r.stdout + r.stderr)
+    os.replace(tmp, CALIB_LIB)
+    if verbose:
+        print(f"built {CALIB_LIB}")
     return LIB
 
 

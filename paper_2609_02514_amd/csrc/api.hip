@@ -64,6 +64,7 @@ struct acespec_ctx {
   float2 *rot = nullptr;      // RoPE (cos, sin) per tree row and frequency, per step
   float *tile_max = nullptr;  // LM-head row maxima per column tile
   uint32_t *cand = nullptr;   // vocabulary kernel: threshold-bin candidates per row
+  int32_t *rowflag = nullptr; // vocabulary kernel: per-row data-error code (0 = none)
   TreeMeta meta{};
   // timing
   bool timing = false;
@@ -124,6 +125,13 @@ int check_params(const acespec_params *p, int V) {
   if (p->top_k < 1 || p->top_k > 256 || p->top_k > V)
     return fail(ACESPEC_EINVAL, "top_k must be in [1, min(256, vocab)] (got %d)", p->top_k);
   return ACESPEC_OK;
+}
+
+// log2(e) / T in double, handed to the vocabulary kernel as a float pair.
+void set_temperature(VocabArgs &va, float T) {
+  const double c = 1.4426950408889634074 / (double)T;
+  va.c_hi = (float)c;
+  va.c_lo = (float)(c - (double)va.c_hi);
 }
 
 int check_outputs(const acespec_outputs *o) {
@@ -192,6 +200,7 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   va.ntile = ntile;
   va.cand = ctx->cand;
   va.cand_cap = kCandCap;
+  va.rowflag = ctx->rowflag;
   va.u = uniforms;
   va.tok = meta.tok;
   va.par = meta.par;
@@ -200,7 +209,7 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   va.rows = R;
   va.V = V;
   va.k = p->top_k;
-  va.inv_T = 1.0f / p->temperature;
+  set_temperature(va, p->temperature);
   va.top_p = p->top_p;
   va.accept = o->accept;
   va.resample = o->resample_token;
@@ -209,9 +218,8 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   va.topk_probs = o->topk_probs;
   RUN(K_VOCAB, launch_vocab(va, stream));
   RUN(K_WALK, launch_walk(meta.tok, meta.par, meta.depth, o->accept, o->resample_token,
-                          o->bonus_token, B,
-                          n1, o->acc_prefix_len, o->path, o->path_len, o->next_token,
-                          o->sibling_hit, stream));
+                          o->bonus_token, ctx->rowflag, B, n1, o->acc_prefix_len, o->path,
+                          o->path_len, o->next_token, o->sibling_hit, o->status, stream));
   return ACESPEC_OK;
 }
 
@@ -246,6 +254,7 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   va.ntile = ntile;
   va.cand = ctx->cand;
   va.cand_cap = kCandCap;
+  va.rowflag = ctx->rowflag;
   va.u = uniforms;
   va.tok = draft;
   va.par = nullptr;
@@ -254,7 +263,7 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   va.rows = R;
   va.V = V;
   va.k = p->top_k;
-  va.inv_T = 1.0f / p->temperature;
+  set_temperature(va, p->temperature);
   va.top_p = p->top_p;
   va.accept = o->accept;
   va.resample = o->resample_token;
@@ -262,9 +271,9 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   va.topk_ids = o->topk_ids;
   va.topk_probs = o->topk_probs;
   RUN(K_VOCAB, launch_vocab(va, stream));
-  RUN(K_WALK, launch_walk_tail(o->accept, o->resample_token, draft, R, chain_len, V,
-                               o->acc_prefix_len, o->path, o->path_len, o->next_token,
-                               o->sibling_hit, o->status, stream));
+  RUN(K_WALK, launch_walk_tail(o->accept, o->resample_token, draft, ctx->rowflag, R,
+                               chain_len, V, o->acc_prefix_len, o->path, o->path_len,
+                               o->next_token, o->sibling_hit, o->status, stream));
   return ACESPEC_OK;
 }
 
@@ -296,9 +305,6 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       return fail(ACESPEC_EINVAL, "n_heads must be a positive multiple of n_kv_heads");
     if (d.d_ff < 64 || d.d_ff % 64 || (d.n_heads * d.head_dim) % 64)
       return fail(ACESPEC_EUNSUPPORTED, "d_ff and n_heads*head_dim must be multiples of 64");
-    const int G = d.n_heads / d.n_kv_heads;
-    if ((G * (max_nodes + 1) + 15) / 16 > 32)
-      return fail(ACESPEC_EUNSUPPORTED, "(n_heads/n_kv_heads)*(max_nodes+1) must be <= 512");
     if (!(d.rope_base > 0.f) || !(d.rms_eps >= 0.f))
       return fail(ACESPEC_EINVAL, "rope_base > 0 and rms_eps >= 0 required");
   }
@@ -317,7 +323,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   struct Part { size_t bytes; void **dst; };
   void *p_x = nullptr, *p_logits = nullptr, *p_po = nullptr, *p_pml = nullptr, *p_if = nullptr;
   void *p_qkv = nullptr, *p_gpart = nullptr, *p_rot = nullptr, *p_tmax = nullptr,
-       *p_cand = nullptr;
+       *p_cand = nullptr, *p_rflag = nullptr;
   void *p_tok = nullptr, *p_par = nullptr, *p_pos = nullptr, *p_depth = nullptr,
        *p_anc = nullptr, *p_S = nullptr;
   std::vector<Part> parts = {
@@ -330,6 +336,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
       {R * (size_t)d.vocab * 4, &p_logits},
       {R * (size_t)((d.vocab + 127) / 128) * 4, &p_tmax},
       {R * (size_t)kCandCap * 4, &p_cand},
+      {R * 4, &p_rflag},
       {(size_t)c->part_cap * 4, &p_po},
       {(size_t)c->part_cap / (layers ? d.head_dim : 1) * 2 * 4, &p_pml},
       {layers ? (size_t)d.head_dim / 2 * 8 : 0, &p_if},
@@ -366,6 +373,7 @@ int acespec_create(const acespec_model_desc *desc, int max_batch, int max_nodes,
   c->rot = (float2 *)p_rot;
   c->tile_max = (float *)p_tmax;
   c->cand = (uint32_t *)p_cand;
+  c->rowflag = (int32_t *)p_rflag;
   c->meta.tok = (int32_t *)p_tok;
   c->meta.par = (int32_t *)p_par;
   c->meta.pos = (int32_t *)p_pos;
@@ -501,11 +509,22 @@ int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_
                       const int32_t *path_len, const int32_t *status, int B, int N,
                       int32_t *new_prefix_len, hipStream_t stream) {
   g_err.clear();
-  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
-  if (ctx->d.n_layers < 1) return fail(ACESPEC_EINVAL, "the model has no layers (no KV cache)");
   if (!kv || !kv->k || !kv->v || !kv->prefix_len || !path || !path_len || !new_prefix_len)
     return fail(ACESPEC_EINVAL, "a required pointer is NULL (only status may be)");
-  if (B < 1 || B > ctx->max_batch)
+  if (B < 1) return fail(ACESPEC_EINVAL, "B must be >= 1 (got %d)", B);
+  {
+    // The kernel's workgroups read prefix_len[b] while one of them writes
+    // new_prefix_len[b]: the two arrays must be distinct memory.
+    const uintptr_t a0 = (uintptr_t)kv->prefix_len, n0 = (uintptr_t)new_prefix_len;
+    const uintptr_t bytes = (uintptr_t)B * sizeof(int32_t);
+    if (a0 < n0 + bytes && n0 < a0 + bytes)
+      return fail(ACESPEC_EINVAL,
+                  "new_prefix_len overlaps kv->prefix_len: give it its own buffer and copy "
+                  "it over after the call");
+  }
+  if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
+  if (ctx->d.n_layers < 1) return fail(ACESPEC_EINVAL, "the model has no layers (no KV cache)");
+  if (B > ctx->max_batch)
     return fail(ACESPEC_EINVAL, "B must be in [1, %d] (got %d)", ctx->max_batch, B);
   if (N < 0 || N > ctx->max_nodes)
     return fail(ACESPEC_EINVAL, "N must be in [0, %d] (got %d)", ctx->max_nodes, N);

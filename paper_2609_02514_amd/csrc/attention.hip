@@ -128,16 +128,21 @@ template <int HD, int NW, int UPW, int NST>
 __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     const f16 *__restrict__ qin, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
     TreeMeta meta, f16 *__restrict__ out, float *__restrict__ part_o,
-    float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit) {
+    float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit, int tpg) {
   constexpr int KSTEPS = HD / 32, NB = HD / 16;
   constexpr int STAGE = 2 * KC * HD;     // elements: K [KC][HD], then V^T [HD][KC]
   constexpr int L_DMA = HD / 4 / NW;     // DMA instructions per wave per chunk
   static_assert(NST >= 3, "the widening runs one stage ahead of the MFMAs");
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
 
-  const int split = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int g = blockIdx.y, b = blockIdx.z;
   const int G = H / Hkv, QR = G * n1;
-  const int ntiles = (QR + 15) / 16;
+  // Query groups: when the query rows of a kv head need more tiles than one workgroup
+  // holds, consecutive groups of tpg tiles go to separate workgroups (each streams the
+  // key range once); tbase is this group's first tile.
+  const int all_tiles = (QR + 15) / 16, nqg = (all_tiles + tpg - 1) / tpg;
+  const int split = blockIdx.x / nqg, tbase = (blockIdx.x - split * nqg) * tpg;
+  const int ntiles = min(tpg, all_tiles - tbase);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   // With several tiles per wave, a last round of only a few tiles would leave the waves
@@ -171,13 +176,13 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
 #pragma unroll
   for (int t = 0; t < UPW; ++t) {
     const int tile = (split_last && t == QS) ? NW * QS + ((wave - qbase) >> 2) : wave + NW * t;
-    int qi = tile * 16 + lr;   // (slot QS of a wave without a quarter unit: unused)
+    int qi = (tbase + tile) * 16 + lr;   // (slot QS of a wave without a quarter unit: unused)
     qi = qi < 0 ? 0 : (qi < QR ? qi : QR - 1);
     const int r = qi / G, h = g * G + (qi - r * G);
     const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
     // padding rows of the last tile multiply zeros (their outputs are dropped; zero
     // operands keep the MFMA's switching, and so its power draw, down)
-    const bool pad = tile * 16 + lr >= QR;
+    const bool pad = (tbase + tile) * 16 + lr >= QR;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
       const f16x8 v = *(const f16x8 *)(qp + s * 32 + lg * 8);
@@ -383,7 +388,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
         wj[j] = mj[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mj[j] - M);
         L += wj[j] * mml[((q0 + j) * 16 + lr) * 2 + 1];
       }
-      const int qi = tile * 16 + lr;
+      const int qi = (tbase + tile) * 16 + lr;
       if (qi < QR) {
         const int r = qi / G, h = g * G + (qi - r * G);
 #pragma unroll
@@ -422,7 +427,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     const int tile = wave + NW * t;
     if (tile >= ntiles || (split_last && t == QS)) break;
     const float l = rows4_sum(l_run[t]);
-    const int qi = tile * 16 + lr;
+    const int qi = (tbase + tile) * 16 + lr;
     if (qi >= QR) continue;
     const int r = qi / G, h = g * G + (qi - r * G);
     if (nsplit == 1) {
@@ -524,10 +529,10 @@ template <int HD> struct AttnCfg { static constexpr int NST = 4; };
 template <int HD, int NW, int UPW>
 void launch_mfma(dim3 grid, hipStream_t s, const f16 *q, const bf16 *ck, const bf16 *cv,
                  const TreeMeta &meta, f16 *out, float *po, float *pml, int n1, int H, int Hkv,
-                 int capacity, int nsplit) {
+                 int capacity, int nsplit, int tpg) {
   hipLaunchKernelGGL((tree_attn_mfma_kernel<HD, NW, UPW, AttnCfg<HD>::NST>), grid,
                      dim3(NW * 64), 0, s, q, ck, cv, meta, out, po, pml, n1, H, Hkv,
-                     capacity, nsplit);
+                     capacity, nsplit, tpg);
 }
 
 }  // namespace
@@ -541,7 +546,12 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
                                   int Hkv, int hd, int capacity, int cus, hipStream_t s,
                                   int *nsplit_used) {
   const int G = H / Hkv, QR = G * n1;
-  const int tiles = (QR + 15) / 16;
+  const int all_tiles = (QR + 15) / 16;
+  // A workgroup takes at most 32 query tiles (8 waves of up to 4); beyond that the tiles
+  // are dealt to ceil(tiles / 32) query groups of equal size (a 64-node tree under 8
+  // query heads per kv head: 520 rows, two groups of 17 tiles).
+  const int nqg = (all_tiles + 31) / 32;
+  const int tiles = (all_tiles + nqg - 1) / nqg;
   // Up to 16 tiles: 16 waves, one tile per wave, the others widen (measured fastest on
   // the 8B shape: 5 tiles); more tiles: 8 waves with up to 4 tiles each.
   const int nw = tiles <= 16 ? 16 : 8;
@@ -550,17 +560,17 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
   // Key splits so that every resident workgroup slot of the chip gets work (one 16-wave
   // workgroup per CU; two 8-wave ones at head_dim 64), keeping at least 4 chunks per split.
   const int slots = cus * (nw == 8 && hd == 64 ? 2 : 1);
-  const int items = B * Hkv;
+  const int items = B * Hkv * nqg;
   const int nchunks = capacity / KC;
   int nsplit = (slots + items - 1) / items;
   nsplit = nsplit < nchunks / 4 ? nsplit : nchunks / 4;
   if (nsplit < 1) nsplit = 1;
-  while (nsplit > 1 && (long long)items * nsplit * QR * hd > part_capacity) --nsplit;
+  while (nsplit > 1 && (long long)B * Hkv * nsplit * QR * hd > part_capacity) --nsplit;
   *nsplit_used = nsplit;
-  const dim3 grid(nsplit, Hkv, B);
+  const dim3 grid(nsplit * nqg, Hkv, B);
 #define GO(HD_, NW_, UPW_)                                                                \
   launch_mfma<HD_, NW_, UPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,  \
-                              capacity, nsplit)
+                              capacity, nsplit, tiles)
   // (more than 16 tiles means at least 3 a wave)
   if (hd == 128) {
     if (nw == 16) GO(128, 16, 1);

@@ -45,6 +45,12 @@ AS_DEVICE uint32_t f32_key(float f) {
   return u ^ ((uint32_t)((int32_t)u >> 31) | 0x80000000u);
 }
 
+// Running maximum that turns any non-finite value (NaN or +-inf) into +inf, so that a
+// maximum over logits also reports whether one of them overflowed.
+AS_DEVICE float max_or_inf(float m, float v) {
+  return fabsf(v) <= 3.402823466e38f ? fmaxf(m, v) : __builtin_inff();
+}
+
 AS_DEVICE float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
@@ -249,13 +255,18 @@ struct VocabArgs {
   int ntile;
   uint32_t *cand;           // [rows, cand_cap] scratch for threshold-bin candidates, or NULL
   int cand_cap;
+  int32_t *rowflag;         // [rows] out: 0, ACESPEC_EBADDRAFT or ACESPEC_ENONFINITE
   const float *u;           // [rows, 3]
   const int32_t *tok;       // [rows] token of each row (children look theirs up here)
   const int32_t *par;       // [rows] parent row within the session, -1 for the root
   int n1;                   // rows per session (1 for the tail)
   int tail;                 // 1: each row is the parent of one drafted token tok[row]
   int rows, V, k;
-  float inv_T, top_p;
+  // log2(e) / T as an unevaluated pair of floats (c_hi + c_lo, from double on the host):
+  // a single fp32 factor would tilt every weight exp2(x c) by x times its rounding error,
+  // a systematic shift of the cumulative masses the inverse CDFs read
+  float c_hi, c_lo;
+  float top_p;
   uint8_t *accept;
   int32_t *resample;
   int32_t *bonus;
@@ -264,11 +275,13 @@ struct VocabArgs {
 };
 hipError_t launch_vocab(const VocabArgs &a, hipStream_t s);
 
+// The walk also folds the rows' data-error codes (rowflag) into status[b] of sessions
+// whose tree was valid.
 hipError_t launch_walk(const int32_t *tok, const int32_t *par, const int32_t *depth,
                        const uint8_t *accept, const int32_t *resample, const int32_t *bonus,
-                       int B, int n1,
-                       int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
-                       int32_t *next_token, uint8_t *sibling_hit, hipStream_t s);
+                       const int32_t *rowflag, int B, int n1, int32_t *acc_prefix_len,
+                       int32_t *path, int32_t *path_len, int32_t *next_token,
+                       uint8_t *sibling_hit, int32_t *status, hipStream_t s);
 
 // Algorithm 1 COMPACT_KV: moves the root and kept rows of each session to the slots
 // following its prefix; new_len[b] = prefix_len[b] + 1 + path_len[b], or -1 (nothing moved)
@@ -280,7 +293,8 @@ hipError_t launch_commit_kv(T *ck, T *cv, const int32_t *prefix_len, const int32
                             hipStream_t s);
 
 hipError_t launch_walk_tail(const uint8_t *accept, const int32_t *resample,
-                            const int32_t *draft, int R, int chain_len, int V,
+                            const int32_t *draft, const int32_t *rowflag, int R,
+                            int chain_len, int V,
                             int32_t *acc_prefix_len, int32_t *path,
                             int32_t *path_len, int32_t *next_token, uint8_t *sibling_hit,
                             int32_t *status, hipStream_t s);

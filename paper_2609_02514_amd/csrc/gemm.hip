@@ -354,16 +354,17 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   if constexpr (EPI == acespec::EPI_F32_MAX) {
     // row maxima over this tile's columns (padding columns repeat the last real one):
     // over the wave's blocks in registers, its 16 column lanes by shuffles, then the
-    // WNN waves of a row through LDS; tmax holds [M][nt]
+    // WNN waves of a row through LDS; tmax holds [M][nt].  A non-finite logit makes its
+    // tile's maximum +inf, which the vocabulary kernel reports.
     __syncthreads();  // every wave is past the ring
     float *red = (float *)smem;  // [WNN][TBM]
 #pragma unroll
     for (int ii = 0; ii < WTM; ++ii)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        float m = acc[ii][0][e];
+        float m = -INFINITY;
 #pragma unroll
-        for (int j = 1; j < WTN; ++j) m = fmaxf(m, acc[ii][j][e]);
+        for (int j = 0; j < WTN; ++j) m = max_or_inf(m, acc[ii][j][e]);
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
         if (lr == 0) red[wn * TBM + wm * WTM * 16 + ii * 16 + lk * 4 + e] = m;
@@ -411,7 +412,7 @@ __global__ __launch_bounds__(256) void tile_fixup_kernel(const float *__restrict
   }
   if constexpr (EPI == acespec::EPI_F32_MAX) {
     // the CW threads of a tile row are CW consecutive lanes of one wave (CW divides 64)
-    float m = fmaxf(fmaxf(a.x, a.y), fmaxf(a.z, a.w));
+    float m = max_or_inf(max_or_inf(max_or_inf(max_or_inf(-INFINITY, a.x), a.y), a.z), a.w);
 #pragma unroll
     for (int o = 1; o < CW; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
     if (row >= M) return;

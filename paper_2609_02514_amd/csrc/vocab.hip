@@ -13,7 +13,8 @@
 //   accept[n] = u0 * Q(x) < p_r(x)         (u0 < min(1, p/q)),
 //   resample[n] = inverse CDF of max(0, p_r - Q) at u1 (of p_r if that has no mass).
 //
-// Arithmetic: e = exp2((z - max) * log2(e) / T) in fp32; probability mass is summed in
+// Arithmetic: e = exp2((z - max) * log2(e) / T) in fp32 (the factor log2(e) / T and the
+// nucleus normaliser each carried as a pair of floats); probability mass is summed in
 // 2^-40 fixed point (64-bit integers), so every reduction is exact, order independent
 // and run-to-run deterministic.  The nucleus and top-k thresholds are found by a radix
 // select on the order-preserving 32-bit key of z (12 + 11 + 9 bits, histograms in LDS
@@ -36,7 +37,6 @@ constexpr int NWV = VT / 64;        // waves
 constexpr int SEG = 256;            // ids per segment (one float4 per lane)
 constexpr int SEGMAX = 1024;        // vocab <= 262144
 constexpr int KMAX = 256;
-constexpr float LOG2E = 1.4426950408889634f;
 
 typedef unsigned long long u64;
 
@@ -72,6 +72,7 @@ struct VSmem {
   u64 above_p;
   uint32_t above_k;
   int sel_p, sel_k;
+  int flag;                // data-error code of the row (0 = none)
 };
 
 AS_DEVICE u64 fixw(float v) { return __float2ull_rn(v * AS_FX_SCALE); }
@@ -170,19 +171,26 @@ struct Sel {
   uint32_t above_k;        // count strictly above tau_k
   uint32_t j_p, j_k;       // tied ids (ascending) kept at the thresholds
   uint32_t c_p, c_k;       // tie counts at the thresholds
-  float M, c;              // row max, log2(e) / T
-  float invSN;             // 1 / nucleus mass (fixed point units)
+  float M;                 // row max
+  float c_hi, c_lo;        // log2(e) / T as a float pair
+  float inv_hi, inv_lo;    // 1 / nucleus mass (fixed point units) as a float pair
 };
 
 // The raw v_exp_f32: for exponents >= -126 it is exactly exp2f (whose extra steps only
 // rescale subnormal results), and anything below 2^-41 rounds to 0 in fixed point anyway.
+// The exponent (z - M) log2(e) / T takes the factor as a float pair, so its error is the
+// rounding of z - M and of the final sum only (random from element to element, not a
+// tilt of the whole distribution).
 AS_DEVICE float elem_e(float z, const Sel &s) {
-  return __builtin_amdgcn_exp2f((z - s.M) * s.c);
+  const float d = z - s.M;
+  return __builtin_amdgcn_exp2f(fmaf(d, s.c_hi, d * s.c_lo));
 }
 
-// p_r of one element given its nucleus membership.
+// p_r of one element given its nucleus membership: the weight's fixed-point value times
+// 1 / (nucleus mass), the latter again as a float pair.
 AS_DEVICE float elem_p(float z, bool in, const Sel &s) {
-  return in ? fixw_f(elem_e(z, s)) * s.invSN : 0.f;
+  const float f = fixw_f(elem_e(z, s));
+  return in ? fmaf(f, s.inv_hi, f * s.inv_lo) : 0.f;
 }
 
 // Nucleus / top-k membership given the element's rank among ids tied at the threshold.
@@ -332,24 +340,54 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
   const float *z = a.logits + (size_t)row * V;
   const int nseg = (V + SEG - 1) / SEG;
 
-  // ---- pass 0: row max -----------------------------------------------------------
+  // ---- pass 0: row max (+inf when a logit is not finite) -------------------------------
   float mx = -INFINITY;
+  if (tid == 0) sm.flag = 0;
   if (a.tile_max) {  // the LM head's epilogue left the row's maximum per column tile
     const float *tm = a.tile_max + (size_t)row * a.ntile;
-    for (int t = tid; t < a.ntile; t += VT) mx = fmaxf(mx, tm[t]);
+    for (int t = tid; t < a.ntile; t += VT) mx = max_or_inf(mx, tm[t]);
   } else {
     for (RowStream rs(z, V, tid * 4); rs.more(); rs.advance()) {
       rs.prefetch();
-      const int i0 = rs.i0;
       const float4 (&vv)[VR] = rs.cur;
 #pragma unroll
       for (int u = 0; u < VR; ++u)
-        mx = fmaxf(fmaxf(mx, fmaxf(vv[u].x, vv[u].y)), fmaxf(vv[u].z, vv[u].w));
+        mx = max_or_inf(max_or_inf(max_or_inf(max_or_inf(mx, vv[u].x), vv[u].y), vv[u].z),
+                        vv[u].w);
     }
   }
   Sel sel;
   sel.M = block_max(mx, sm);
-  sel.c = LOG2E * a.inv_T;
+  sel.c_hi = a.c_hi;
+  sel.c_lo = a.c_lo;
+  const bool tail = a.tail != 0;
+  const int b = row / a.n1, r = row - b * a.n1;
+  const size_t srow0 = (size_t)b * a.n1;
+  if (!(sel.M <= 3.402823466e38f)) {
+    // A logit of this row is NaN or infinite (an activation overflowed upstream): the row
+    // gets no decisions, the session's status reports it.  Outputs stay defined.
+    const int k = a.k;
+    if (tid < k) {
+      a.topk_ids[(size_t)row * k + tid] = -1;
+      a.topk_probs[(size_t)row * k + tid] = 0.f;
+    }
+    if (tid == 0) {
+      a.bonus[row] = -1;
+      a.rowflag[row] = ACESPEC_ENONFINITE;
+      if (!tail && r == 0) {
+        a.accept[row] = 1;
+        a.resample[row] = -1;
+      }
+    }
+    const int c_lo = tail ? 0 : r + 1, c_hi = tail ? 1 : a.n1;
+    for (int ci = c_lo + tid; ci < c_hi; ci += VT) {
+      const int child = tail ? row : (int)(srow0 + ci);
+      if (!tail && a.par[srow0 + ci] != r) continue;
+      a.accept[child] = 0;
+      a.resample[child] = -1;
+    }
+    return;
+  }
 
   // ---- pass 1: total mass, 12-bit histograms ---------------------------------------
   for (int i = tid; i < 4096; i += VT) {
@@ -491,7 +529,9 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
     sel.j_p = (uint32_t)j;
     sel.j_k = (uint32_t)(K - ak3);
     const u64 SN = ap3 + j * w_tau;
-    sel.invSN = (float)(1.0 / (double)SN);
+    const double inv = 1.0 / (double)SN;
+    sel.inv_hi = (float)inv;
+    sel.inv_lo = (float)(inv - (double)sel.inv_hi);
   }
   __syncthreads();
 
@@ -533,9 +573,6 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
   }
 
   // ---- pass 4: id-ordered segments: masses of p_r and of the residual, top-k ids ----------
-  const bool tail = a.tail != 0;
-  const int b = row / a.n1, r = row - b * a.n1;
-  const size_t srow0 = (size_t)b * a.n1;
   bool has_child = tail;
   if (!tail) {
     for (int c = r + 1; c < a.n1; ++c) has_child |= a.par[srow0 + c] == r;
@@ -548,6 +585,8 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
   const float *q = dense_q ? a.q + (size_t)row * V : nullptr;
   // The VU segments of a step are loaded before any is used.  Past the end of the row the
   // last float4 is loaded again (unconditional loads); those lanes are not valid below.
+  // Every draft probability read is checked: NaN, infinite or negative flags the row.
+  bool badq = false;
   for (int s0 = wave; s0 < nseg; s0 += NWV * VU) {
   float4 z4u[VU], q4u[VU];
 #pragma unroll
@@ -586,7 +625,10 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
       const bool inn = in_nucleus(key[j], rp[j], sel);
       const float p = elem_p(zz[j], inn, sel);
       sp_ += fixw(p);
-      if (resid) sr_ += fixw(fmaxf(p - qq[j], 0.f));
+      if (resid) {
+        badq |= !(qq[j] >= 0.f && qq[j] <= 3.402823466e38f);
+        sr_ += fixw(fmaxf(p - qq[j], 0.f));
+      }
       if (in_topk(key[j], rk[j], sel)) {
         const uint32_t slot = atomicAdd(&sm.ncand, 1u);
         if (slot < KMAX) {
@@ -604,7 +646,7 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
     }
   }
   }
-  __syncthreads();
+  if (__syncthreads_or(badq) && tid == 0) sm.flag = ACESPEC_EBADDRAFT;
   // exclusive prefixes over segments
   u64 Ptot, Rtot;
   {
@@ -707,6 +749,7 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
       }
       const float px = elem_p(zx, in_nucleus(kx, rx, sel), sel);
       const float qx = dense_q ? q[x] : a.q_scalar[child];
+      if (!dense_q && !(qx >= 0.f && qx <= 1.f) && lane == 0) sm.flag = ACESPEC_EBADDRAFT;
       const float u0 = u[(size_t)child * 3 + 0], u1 = u[(size_t)child * 3 + 1];
       const bool acc = u0 * qx < px;
       int res = -1;
@@ -727,6 +770,8 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
       }
     }
   }
+  __syncthreads();
+  if (tid == 0) a.rowflag[row] = sm.flag;
 }
 
 }  // namespace

@@ -5,7 +5,8 @@
 // of the same node (the outcome w = (pi, x_resampled) queried in the drafted tree): a hit
 // continues down that sibling, a miss ends the path with the resampled token.  A node
 // without children ends the path with its bonus token.  Also derives, per row, the
-// number of leading accepted nodes on its root-to-row path.
+// number of leading accepted nodes on its root-to-row path, and reports a data error the
+// vocabulary kernel found in any of the session's rows in its status.
 #include "common.h"
 
 namespace {
@@ -20,11 +21,13 @@ constexpr int WALK_THREADS = 128;  // one thread per tree row (at most 65 rows)
 __global__ __launch_bounds__(WALK_THREADS) void walk_kernel(
     const int32_t *__restrict__ tok, const int32_t *__restrict__ par,
     const int32_t *__restrict__ depth, const uint8_t *__restrict__ accept,
-    const int32_t *__restrict__ resample, const int32_t *__restrict__ bonus, int B, int n1,
-    int32_t *__restrict__ acc_prefix_len, int32_t *__restrict__ path,
-    int32_t *__restrict__ path_len, int32_t *__restrict__ next_token,
-    uint8_t *__restrict__ sibling_hit) {
+    const int32_t *__restrict__ resample, const int32_t *__restrict__ bonus,
+    const int32_t *__restrict__ rowflag, int B, int n1, int32_t *__restrict__ acc_prefix_len,
+    int32_t *__restrict__ path, int32_t *__restrict__ path_len,
+    int32_t *__restrict__ next_token, uint8_t *__restrict__ sibling_hit,
+    int32_t *__restrict__ status) {
   constexpr int NONE = 1 << 30;
+  __shared__ int s_flag;
   __shared__ int s_par[WALK_THREADS], s_tok[WALK_THREADS], s_rs[WALK_THREADS];
   __shared__ int s_bonus[WALK_THREADS], s_main[WALK_THREADS], s_jump[WALK_THREADS];
   __shared__ int s_f[WALK_THREADS];
@@ -43,8 +46,11 @@ __global__ __launch_bounds__(WALK_THREADS) void walk_kernel(
   s_main[r] = NONE;
   s_jump[r] = p < 0 ? 0 : p;
   s_f[r] = ok ? NONE : d;
+  if (r == 0) s_flag = 0;
   __syncthreads();
   if (p >= 0) atomicMin(&s_main[p], r);
+  // data-error codes of the session's rows (negative; the smallest, ENONFINITE, wins)
+  if (in && rowflag[base + r] != 0) atomicMin(&s_flag, rowflag[base + r]);
   for (int round = 0; round < 7; ++round) {
     __syncthreads();
     const int jr = s_jump[r];
@@ -55,8 +61,10 @@ __global__ __launch_bounds__(WALK_THREADS) void walk_kernel(
     s_jump[r] = jj;
   }
   if (in) acc_prefix_len[base + r] = min(d, s_f[r] - 1);
-  __syncthreads();  // main children complete
+  __syncthreads();  // main children and row flags complete
   if (r != 0) return;
+  // a valid tree (tree prep wrote OK) with a data error in one of its rows
+  if (s_flag != 0 && status[b] == ACESPEC_OK) status[b] = s_flag;
   int cur = 0, len = 0, hit = 0, nxt = -1;
   while (true) {  // every step moves to a higher row, so at most n1 steps
     const int main_c = s_main[cur];
@@ -84,7 +92,8 @@ __global__ __launch_bounds__(WALK_THREADS) void walk_kernel(
 // LM-head tail: chains of chain_len rows, row i the parent of drafted token i.
 __global__ void walk_tail_kernel(const uint8_t *__restrict__ accept,
                                  const int32_t *__restrict__ resample,
-                                 const int32_t *__restrict__ draft, int nchains, int chain_len,
+                                 const int32_t *__restrict__ draft,
+                                 const int32_t *__restrict__ rowflag, int nchains, int chain_len,
                                  int V, int32_t *__restrict__ acc_prefix_len,
                                  int32_t *__restrict__ path, int32_t *__restrict__ path_len,
                                  int32_t *__restrict__ next_token,
@@ -95,16 +104,18 @@ __global__ void walk_tail_kernel(const uint8_t *__restrict__ accept,
   int i = 0;
   while (i < chain_len && accept[base + i]) ++i;
   bool ok = true;
+  int flag = 0;
   for (int j = 0; j < chain_len; ++j) {
     const int t = draft[base + j];
     ok = ok && t >= 0 && t < V;
+    flag = min(flag, rowflag[base + j]);
     acc_prefix_len[base + j] = i < j + 1 ? i : j + 1;
     path[base + j] = j < i ? j : -1;
   }
   path_len[c] = i;
   next_token[c] = i < chain_len ? resample[base + i] : -1;
   sibling_hit[c] = 0;
-  status[c] = ok ? ACESPEC_OK : ACESPEC_EBADTREE;
+  status[c] = ok ? flag : ACESPEC_EBADTREE;
 }
 
 }  // namespace
@@ -113,24 +124,26 @@ namespace acespec {
 
 hipError_t launch_walk(const int32_t *tok, const int32_t *par, const int32_t *depth,
                        const uint8_t *accept,
-                       const int32_t *resample, const int32_t *bonus, int B, int n1,
-                       int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
-                       int32_t *next_token, uint8_t *sibling_hit, hipStream_t s) {
+                       const int32_t *resample, const int32_t *bonus,
+                       const int32_t *rowflag, int B, int n1, int32_t *acc_prefix_len,
+                       int32_t *path, int32_t *path_len, int32_t *next_token,
+                       uint8_t *sibling_hit, int32_t *status, hipStream_t s) {
   if (n1 > WALK_THREADS) return hipErrorInvalidValue;
   hipLaunchKernelGGL(walk_kernel, dim3(B), dim3(WALK_THREADS), 0, s, tok, par, depth, accept,
-                     resample, bonus, B, n1, acc_prefix_len, path, path_len, next_token,
-                     sibling_hit);
+                     resample, bonus, rowflag, B, n1, acc_prefix_len, path, path_len,
+                     next_token, sibling_hit, status);
   return hipGetLastError();
 }
 
 hipError_t launch_walk_tail(const uint8_t *accept, const int32_t *resample,
-                            const int32_t *draft, int R, int chain_len, int V,
+                            const int32_t *draft, const int32_t *rowflag, int R,
+                            int chain_len, int V,
                             int32_t *acc_prefix_len, int32_t *path, int32_t *path_len,
                             int32_t *next_token, uint8_t *sibling_hit, int32_t *status,
                             hipStream_t s) {
   const int nchains = R / chain_len;
   hipLaunchKernelGGL(walk_tail_kernel, dim3((nchains + 63) / 64), dim3(64), 0, s, accept,
-                     resample, draft, nchains, chain_len, V, acc_prefix_len, path, path_len,
+                     resample, draft, rowflag, nchains, chain_len, V, acc_prefix_len, path, path_len,
                      next_token, sibling_hit, status);
   return hipGetLastError();
 }

@@ -4,21 +4,33 @@ inputs, and classifies every disagreement.
 Tolerances (from the target stated for this hot path):
   * logits: per row, max |z_gpu - z_ref| / max |z_ref| <= 2e-2 (bf16 weights and
     activations; fp32 path and LM-head-only runs are held to tighter bounds by the tests);
-  * decisions (accept, acc_prefix_len, resample, bonus, top-k ids): compared with the
-    oracle's verify stage run on the GPU's own logits, identical on >= 99.9 % of nodes,
-    every mismatch explained by a boundary case:
+  * decisions (accept, resample, bonus, top-k ids and probabilities): the oracle's verify
+    stage is run on the GPU's own logits for EVERY row of every session, and the GPU's
+    decisions must be identical on >= 99.9 % of the checked nodes (a node = one row's
+    payload and bonus, or one child's accept and resample), every mismatch explained by
+    a boundary case of the arithmetic:
       accept      |p/q - u| < 1e-3
       inv. CDF    |C_j / S - u| < 1e-3 at the chosen or a neighbouring id
-      top-p       |C_m - top_p| < 1e-4 (the nucleus edge moves)
+      top-p       |C_m - top_p| < 1e-5 (the nucleus edge moves): the GPU sums each weight
+                  exp2(fp32 exponent) in 2^-40 fixed point, so any partial mass it forms
+                  is within a few 1e-6 of the float64 one (exponent rounding up to
+                  |x| 2^-24 for |x| <= 126, one ulp in exp2, V 2^-41 of fixed point)
       top-k       |p_a - p_b| <= 1e-4 p_a (tie)
-    and the walk is re-derived from the GPU's own per-node decisions exactly.
+    The acceptance prefix lengths and the walk are re-derived from the GPU's own
+    per-node decisions exactly.
+  * informational (reading C22 of the scope): the same decisions against the oracle's
+    verify stage on the oracle's own float64 logits, for the sessions whose forward the
+    oracle ran.
 """
 from __future__ import annotations
 
+import os
 import sys
 import time
+from collections import Counter
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
-from typing import Dict, List, Sequence
+from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 import torch
@@ -26,6 +38,10 @@ import torch
 import synth
 from oracle import model as om
 from oracle import verify as ov
+
+RATE = 1e-3          # at most 0.1 % of the checked nodes may differ
+TOPP_EDGE = 1e-5     # top-p boundary class (see the module docstring)
+THREADS = min(16, os.cpu_count() or 1)
 
 
 def log(msg: str):
@@ -37,6 +53,11 @@ def host(t):
     return t.detach().to("cpu")
 
 
+def parity_seeds(w: synth.Workload, n: int) -> List[int]:
+    """The parity seeds of a workload: its master seed + 100 i, i = 0 .. n-1."""
+    return [w.seed_base + 100 * i for i in range(n)]
+
+
 # ---------------------------------------------------------------------------------------
 # GPU runs
 # ---------------------------------------------------------------------------------------
@@ -46,10 +67,16 @@ def host(t):
 class TreeRun:
     w: synth.Workload
     W: synth.Weights          # device weights
-    batch: synth.Batch        # device inputs
+    batch: synth.Batch        # device inputs (the cache prefix is never written)
     outs: Dict                # host copies of the outputs
     host_in: Dict             # host copies of the inputs the oracle needs
-    sessions: List[int]
+    sessions: List[int]       # sessions whose forward the oracle runs
+
+    def kv_prefix(self, l: int, b: int):
+        """Session b's layer-l cache prefix as float64 [Hkv, S, hd] (keys and values),
+        read from the device cache: the verify step writes only slots >= prefix_len."""
+        S = int(self.host_in["prefix_len"][b])
+        return (om.k_prefix(self.batch.kv_k, l, b, S), om.v_prefix(self.batch.kv_v, l, b, S))
 
 
 def run_tree(w: synth.Workload, seed=None, sessions: Sequence[int] = None, device="cuda",
@@ -61,12 +88,8 @@ def run_tree(w: synth.Workload, seed=None, sessions: Sequence[int] = None, devic
     batch = synth.make_batch(w, device, seed)
     B, n1 = batch.tokens.shape
     sessions = list(range(B)) if sessions is None else list(sessions)
-    # host copies BEFORE the HIP path runs (it writes the tree slots of the cache)
     hin = dict(tokens=host(batch.tokens), parents=host(batch.parents),
-               prefix_len=host(batch.prefix_len), q=host(batch.q), u=host(batch.u),
-               kv={(l, b): (om.k_prefix(batch.kv_k, l, b, int(batch.prefix_len[b])),
-                            om.v_prefix(batch.kv_v, l, b, int(batch.prefix_len[b])))
-                   for l in range(w.L) for b in sessions})
+               prefix_len=host(batch.prefix_len), q=host(batch.q), u=host(batch.u))
     v = verifier or Verifier.for_workload(w)
     ws = v.weights_struct(W)
     outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, device, keep_logits)
@@ -85,8 +108,7 @@ def oracle_tree_logits(run: TreeRun) -> np.ndarray:
     w = run.w
     hin = run.host_in
     return om.forward_tree_batch(run.W, om.dims_of(w), hin["tokens"], hin["parents"],
-                                 hin["prefix_len"], lambda l, b: hin["kv"][(l, b)],
-                                 run.sessions, progress=log)
+                                 hin["prefix_len"], run.kv_prefix, run.sessions, progress=log)
 
 
 # ---------------------------------------------------------------------------------------
@@ -100,135 +122,238 @@ def logits_rel_err(z_gpu: np.ndarray, z_ref: np.ndarray) -> np.ndarray:
 
 
 @dataclass
+class Mismatch:
+    tag: str      # where: b<session>r<row> / c<child> ...
+    what: str     # which decision and the two values
+    cls: str      # boundary class that explains it, or "unexplained"
+
+
+@dataclass
 class Report:
     nodes: int = 0
-    mismatches: List[str] = field(default_factory=list)
-    unexplained: List[str] = field(default_factory=list)
+    mismatches: List[Mismatch] = field(default_factory=list)
 
-    def ok(self, rate=1e-3) -> bool:
-        allowed = max(1, int(rate * self.nodes))
-        return not self.unexplained and len(self.mismatches) <= allowed
+    @property
+    def unexplained(self) -> List[Mismatch]:
+        return [m for m in self.mismatches if m.cls == "unexplained"]
+
+    def add(self, other: "Report"):
+        self.nodes += other.nodes
+        self.mismatches += other.mismatches
+
+    def ok(self, rate=RATE) -> bool:
+        return not self.unexplained and len(self.mismatches) <= int(rate * self.nodes)
+
+    def classes(self) -> Dict[str, int]:
+        return dict(Counter(m.cls for m in self.mismatches))
 
     def __str__(self):
+        agree = 1.0 - len(self.mismatches) / max(1, self.nodes)
         return (f"nodes={self.nodes} mismatches={len(self.mismatches)} "
-                f"unexplained={self.unexplained[:5]} first={self.mismatches[:5]}")
+                f"({100 * agree:.3f} % identical) by class {self.classes()} "
+                f"first={[f'{m.tag}: {m.what} [{m.cls}]' for m in self.mismatches[:6]]}")
 
 
 def _cdf_boundary(w: np.ndarray, u: float, j_a: int, j_b: int, eps=1e-3) -> bool:
     c = np.cumsum(w) / w.sum()
     lo, hi = min(j_a, j_b), max(j_a, j_b)
+    lo, hi = max(0, lo), min(len(c) - 1, hi)
     cand = [c[j] for j in range(max(0, lo - 1), min(len(c), hi + 1))]
     return any(abs(x - u) < eps for x in cand)
 
 
-def _topp_boundary(pt: np.ndarray, top_p: float, eps=1e-4) -> bool:
-    order = ov.sorted_order(pt)
+def _topp_boundary(pt: np.ndarray, order: np.ndarray, top_p: float, eps=TOPP_EDGE) -> bool:
     cs = np.cumsum(pt[order])
     m = int(np.searchsorted(cs, top_p))
     near = [cs[j] for j in range(max(0, m - 1), min(len(cs), m + 2))]
     return any(abs(x - top_p) < eps for x in near)
 
 
-def compare_row_decisions(rep: Report, tag: str, z: np.ndarray, q_par: np.ndarray,
-                          children: List[int], tok: Sequence[int], u: np.ndarray,
-                          T: float, top_p: float, k: int, g: Dict, row_g: int,
-                          child_g: Dict[int, int]):
-    """Oracle verify of one parent row on the GPU's logits vs the GPU's decisions.
+@dataclass
+class RowJob:
+    """One parent or leaf row: its logits, its draft distribution (dense mode) and its
+    children (output index, token, accept uniform, residual uniform, scalar q-hat)."""
+    tag: str
+    gi: int                         # row index in the GPU outputs
+    z: np.ndarray                   # [V] logits the decisions are taken on
+    q: Optional[np.ndarray]         # [V] draft distribution of the children (fp32), or None
+    u_bonus: float
+    children: List[tuple] = field(default_factory=list)   # (gi, x, u0, u1, q_hat)
 
-    g: host GPU outputs; row_g: index of this row in the GPU outputs; child_g maps local
-    child -> GPU output index.  u rows are indexed by local row."""
+
+def _check_row(job: RowJob, g: Dict, T: float, top_p: float, k: int, scalar: bool) -> Report:
+    rep = Report()
+    z = np.asarray(job.z, dtype=np.float64)
+    qd = None if job.q is None else np.asarray(job.q, dtype=np.float64)
     pt = ov.tempered_softmax(z, T)
     p, order, m = ov.nucleus(pt, top_p)
-    topp_edge = _topp_boundary(pt, top_p)
+    edge = None
+
+    def topp_edge():
+        nonlocal edge
+        if edge is None:
+            edge = _topp_boundary(pt, order, top_p)
+        return edge
+
     ids, probs = ov.topk_payload(p, order, k)
     rep.nodes += 1
-    gid = g["topk_ids"][row_g].numpy()
+    gid = g["topk_ids"][job.gi]
     if not np.array_equal(gid, ids):
-        msg = f"{tag}: topk ids"
-        # ids may differ only through exact or near ties of p
         diff = [i for i in range(k) if gid[i] != ids[i]]
-        tie = all(abs(pt[gid[i]] - pt[ids[i]]) <= 1e-4 * pt[ids[i]] for i in diff)
-        rep.mismatches.append(msg)
-        if not tie:
-            rep.unexplained.append(msg)
+        tie = all(0 <= gid[i] < len(pt) and
+                  abs(pt[gid[i]] - pt[ids[i]]) <= 1e-4 * pt[ids[i]] for i in diff)
+        rep.mismatches.append(Mismatch(job.tag, f"topk ids {gid[diff[0]]} vs {ids[diff[0]]}",
+                                       "topk_tie" if tie else "unexplained"))
     else:
-        gp = g["topk_probs"][row_g].numpy().astype(np.float64)
-        if np.abs(gp - probs).max() > 1e-4 and not topp_edge:
-            rep.mismatches.append(f"{tag}: topk probs {np.abs(gp - probs).max():.2e}")
-            rep.unexplained.append(rep.mismatches[-1])
-    j = ov.inverse_cdf(p, float(u[2]) if u.ndim == 1 else float(u[row_g, 2]))
-    gb = int(g["bonus_token"][row_g])
-    ub = float(u[2]) if u.ndim == 1 else float(u[row_g, 2])
-    if gb != j:
-        msg = f"{tag}: bonus {gb} vs {j}"
-        rep.mismatches.append(msg)
-        if not (_cdf_boundary(p, ub, gb, j) or topp_edge):
-            rep.unexplained.append(msg)
+        gp = g["topk_probs"][job.gi].astype(np.float64)
+        err = np.abs(gp - probs).max()
+        if err > 1e-4:
+            rep.mismatches.append(Mismatch(job.tag, f"topk probs {err:.2e}",
+                                           "topp_edge" if topp_edge() else "unexplained"))
+    gb = int(g["bonus_token"][job.gi])
+    if scalar:
+        if gb != -1:
+            rep.mismatches.append(Mismatch(job.tag, f"bonus {gb} in scalar mode", "unexplained"))
+    else:
+        j = ov.inverse_cdf(p, job.u_bonus)
+        if gb != j:
+            cls = ("cdf_boundary" if _cdf_boundary(p, job.u_bonus, gb, j)
+                   else "topp_edge" if topp_edge() else "unexplained")
+            rep.mismatches.append(Mismatch(job.tag, f"bonus {gb} vs {j}", cls))
+    for (ci, x, u0, u1, q_hat) in job.children:
+        rep.nodes += 1
+        ctag = f"{job.tag}c{ci}"
+        g_acc, g_res = bool(g["accept"][ci]), int(g["resample_token"][ci])
+        if scalar:
+            acc = ov.accept_scalar(p, x, q_hat, u0)
+            ratio = p[x] / q_hat if q_hat > 0 else np.inf
+            res = -1
+        else:
+            acc = ov.accept_token(p, qd, x, u0)
+            ratio = p[x] / qd[x] if qd[x] > 0 else np.inf
+            res = ov.residual_sample(p, qd, u1)
+        if g_acc != acc:
+            cls = ("accept_boundary" if abs(ratio - u0) < 1e-3
+                   else "topp_edge" if topp_edge() else "unexplained")
+            rep.mismatches.append(Mismatch(ctag, f"accept {int(g_acc)} vs {int(acc)} "
+                                           f"(p/q={ratio:.6f} u={u0:.6f})", cls))
+        if g_res != res:
+            if scalar:
+                cls = "unexplained"
+            else:
+                rho = np.maximum(p - qd, 0.0)
+                wv = rho if rho.sum() > 0 else p
+                cls = ("cdf_boundary" if _cdf_boundary(wv, u1, g_res, res)
+                       else "topp_edge" if topp_edge() else "unexplained")
+            rep.mismatches.append(Mismatch(ctag, f"resample {g_res} vs {res}", cls))
+    return rep
 
 
-def compare_child(rep: Report, tag: str, z: np.ndarray, qrow: np.ndarray, x: int, u0: float,
-                  u1: float, T: float, top_p: float, g_acc: int, g_res: int):
-    pt = ov.tempered_softmax(z, T)
-    p, order, m = ov.nucleus(pt, top_p)
-    topp_edge = _topp_boundary(pt, top_p)
-    rep.nodes += 1
-    acc = ov.accept_token(p, qrow, x, u0)
-    res = ov.residual_sample(p, qrow, u1)
-    if bool(g_acc) != acc:
-        msg = f"{tag}: accept {g_acc} vs {int(acc)} (p/q={p[x] / max(qrow[x], 1e-300):.6f} u={u0:.6f})"
-        rep.mismatches.append(msg)
-        ratio = p[x] / qrow[x] if qrow[x] > 0 else np.inf
-        if not (abs(ratio - u0) < 1e-3 or topp_edge):
-            rep.unexplained.append(msg)
-    if g_res != res:
-        msg = f"{tag}: resample {g_res} vs {res}"
-        rep.mismatches.append(msg)
-        rho = np.maximum(p - qrow, 0.0)
-        wv = rho if rho.sum() > 0 else p
-        if not (_cdf_boundary(wv, u1, g_res, res) or topp_edge):
-            rep.unexplained.append(msg)
-
-
-def check_tree_decisions(run: TreeRun, z_gpu_rows: Dict[int, np.ndarray]) -> Report:
-    """Oracle verify stage on the GPU's logits for the sampled sessions."""
-    w = run.w
-    hin, g = run.host_in, run.outs
-    B, n1 = hin["tokens"].shape
+def check_rows(jobs: List[RowJob], g: Dict, T: float, top_p: float, k: int,
+               scalar: bool = False) -> Report:
+    """Oracle verify stage on each job's logits against the GPU's decisions, rows in
+    parallel threads (numpy releases the interpreter lock in its vocabulary-wide loops).
+    The sampling parameters are taken as the fp32 values the C ABI carries
+    (acespec_params), i.e. the parameters the GPU actually ran with."""
+    T, top_p = float(np.float32(T)), float(np.float32(top_p))
     rep = Report()
-    for b in run.sessions:
-        toks = [int(t) for t in hin["tokens"][b]]
+    with ThreadPoolExecutor(THREADS) as ex:
+        for r in ex.map(lambda j: _check_row(j, g, T, top_p, k, scalar), jobs):
+            rep.add(r)
+    return rep
+
+
+def _host_outputs(outs: Dict) -> Dict:
+    return {k: (t.numpy() if t is not None else None) for k, t in outs.items()}
+
+
+def tree_jobs(run: TreeRun, z_rows, sessions: Sequence[int], q_hat=None) -> List[RowJob]:
+    """Row jobs of the given sessions.  z_rows(b) -> [N+1, V] logits of session b."""
+    hin = run.host_in
+    B, n1 = hin["tokens"].shape
+    jobs = []
+    for b in sessions:
+        toks = hin["tokens"][b].numpy()
         pars = [int(p) for p in hin["parents"][b]]
         ch = ov.children_of(pars)
-        q = hin["q"][b].numpy().astype(np.float64)
+        q = hin["q"][b].numpy() if hin.get("q") is not None else None
         u = hin["u"][b].numpy().astype(np.float64)
+        z = z_rows(b)
         for r in range(n1):
-            gi = b * n1 + r
-            z = z_gpu_rows[gi]
-            compare_row_decisions(rep, f"b{b}r{r}", z, q[r], ch[r], toks, u[r], w.T, w.top_p,
-                                  w.top_k, g, gi, {})
-            for c in ch[r]:
-                compare_child(rep, f"b{b}c{c}", z, q[r], toks[c], float(u[c, 0]),
-                              float(u[c, 1]), w.T, w.top_p, int(g["accept"][b * n1 + c]),
-                              int(g["resample_token"][b * n1 + c]))
-        # the walk and prefix lengths follow exactly from the GPU's own decisions
-        res = ov.RowResult(accept=g["accept"][b * n1:(b + 1) * n1].numpy(), acc_prefix_len=None,
-                           resample=g["resample_token"][b * n1:(b + 1) * n1].numpy(),
-                           bonus=g["bonus_token"][b * n1:(b + 1) * n1].numpy(), topk_ids=None,
+            kids = [(b * n1 + c, int(toks[c]), float(u[c, 0]), float(u[c, 1]),
+                     float(q_hat[b, c]) if q_hat is not None else None) for c in ch[r]]
+            qr = q[r] if (q is not None and kids and q_hat is None) else None
+            jobs.append(RowJob(f"b{b}r{r}", b * n1 + r, z[r], qr, float(u[r, 2]), kids))
+    return jobs
+
+
+def check_tree_walk(run: TreeRun, sessions: Sequence[int], scalar: bool = False):
+    """The walk, the acceptance prefix lengths and the status of each session follow
+    exactly from the GPU's own per-node decisions."""
+    hin, g = run.host_in, run.outs
+    B, n1 = hin["tokens"].shape
+    for b in sessions:
+        toks = [int(t) for t in hin["tokens"][b]]
+        pars = [int(p) for p in hin["parents"][b]]
+        sl = slice(b * n1, (b + 1) * n1)
+        res = ov.RowResult(accept=g["accept"][sl].numpy(), acc_prefix_len=None,
+                           resample=g["resample_token"][sl].numpy(),
+                           bonus=g["bonus_token"][sl].numpy(), topk_ids=None,
                            topk_probs=None, nucleus_size=None)
         wr = ov.walk(toks, pars, res)
         gl = int(g["path_len"][b])
         gp = g["path"][b].numpy().tolist()
         assert gl == len(wr.path), (b, gl, wr.path)
         assert gp[:gl] == wr.path and all(x == -1 for x in gp[gl:]), (b, gp, wr.path)
-        assert int(g["next_token"][b]) == wr.next_token, (b, int(g["next_token"][b]), wr)
+        assert int(g["next_token"][b]) == (-1 if scalar else wr.next_token), b
         assert int(g["sibling_hit"][b]) == int(wr.sibling_hit)
-        # acc_prefix_len from the GPU accept bits
+        if scalar:
+            assert not wr.sibling_hit
         depth = om.tree_depths(pars)
         acc = [0] * n1
         for r in range(1, n1):
             p_ = pars[r]
             acc[r] = acc[p_] + 1 if (acc[p_] == depth[p_] and res.accept[r]) else acc[p_]
-        assert g["acc_prefix_len"][b * n1:(b + 1) * n1].tolist() == acc
+        assert g["acc_prefix_len"][sl].tolist() == acc, b
         assert int(g["accept"][b * n1]) == 1 and int(g["resample_token"][b * n1]) == -1
-        assert int(g["status"][b]) == 0
+        assert int(g["status"][b]) == 0, (b, int(g["status"][b]))
+
+
+def check_tree_decisions(run: TreeRun, z_gpu_rows: Dict[int, np.ndarray] = None,
+                         sessions: Sequence[int] = None) -> Report:
+    """Oracle verify stage on the GPU's logits (every row of the given sessions; default:
+    every session) and the walk of each, which must follow from the GPU's decisions."""
+    w = run.w
+    B, n1 = run.host_in["tokens"].shape
+    sessions = list(range(B)) if sessions is None else list(sessions)
+    if z_gpu_rows is None:
+        zl = run.outs["logits_out"].numpy()
+        z_rows = lambda b: zl[b * n1:(b + 1) * n1]
+    else:
+        z_rows = lambda b: np.stack([z_gpu_rows[b * n1 + r] for r in range(n1)])
+    g = _host_outputs(run.outs)
+    rep = check_rows(tree_jobs(run, z_rows, sessions), g, w.T, w.top_p, w.top_k)
+    check_tree_walk(run, sessions)
     return rep
+
+
+def agreement_on_oracle_logits(run: TreeRun, z_ref: np.ndarray) -> Report:
+    """Informational: the GPU's decisions against the oracle's verify stage on the
+    oracle's own float64 logits (the forward-sampled sessions)."""
+    w = run.w
+    g = _host_outputs(run.outs)
+    idx = {b: i for i, b in enumerate(run.sessions)}
+    return check_rows(tree_jobs(run, lambda b: z_ref[idx[b]], run.sessions), g, w.T,
+                      w.top_p, w.top_k)
+
+
+def tail_jobs(z: np.ndarray, q: np.ndarray, draft: np.ndarray, u: np.ndarray,
+              rows: Sequence[int], z_row_of=None) -> List[RowJob]:
+    """Row jobs of the LM-head tail: row r is the parent of draft[r].  z is indexed by
+    position in `rows` unless z_row_of maps a row to its z index."""
+    jobs = []
+    for i, r in enumerate(rows):
+        zi = i if z_row_of is None else z_row_of(r)
+        jobs.append(RowJob(f"r{r}", r, z[zi], q[r], float(u[r, 2]),
+                           [(r, int(draft[r]), float(u[r, 0]), float(u[r, 1]), None)]))
+    return jobs

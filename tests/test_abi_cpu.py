@@ -37,3 +37,33 @@ def test_struct_layouts_match_the_header():
 
 def test_last_error_starts_empty():
     assert A.acespec_last_error() == ""
+
+
+def test_status_codes_match_the_header():
+    src = open(os.path.join(ROOT, "include", "acespec.h")).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"\b(ACESPEC_E[A-Z]+)\s*=\s*(-?\d+)", src))
+    assert enum == {"ACESPEC_EINVAL": -1, "ACESPEC_EUNSUPPORTED": -2, "ACESPEC_ENOMEM": -3,
+                    "ACESPEC_EHIP": -4, "ACESPEC_EBADTREE": -5, "ACESPEC_EBADDRAFT": -6,
+                    "ACESPEC_ENONFINITE": -7}
+    for k, v in enum.items():
+        assert getattr(A, k) == v, k
+
+
+def test_commit_rejects_new_prefix_len_aliasing_prefix_len():
+    """acespec_commit_kv's workgroups read prefix_len[b] while one of them writes
+    new_prefix_len[b], so overlapping arrays are refused before anything is launched (no
+    device memory is touched: the pointers below are never dereferenced)."""
+    lib = A.load()
+    base = 0x7F0000001000
+    B, N = 4, 16
+    for new_ptr in (base, base + 8, base - 12):   # same array, inside it, straddling it
+        kv = A.KVCache(0x1000, 0x2000, 64, base)
+        rc = lib.acespec_commit_kv(None, ctypes.byref(kv), 0x3000, 0x4000, None, B, N, new_ptr,
+                                   None)
+        assert rc == A.ACESPEC_EINVAL
+        assert "overlaps" in A.acespec_last_error()
+    # disjoint arrays pass the check and stop at the missing context instead
+    kv = A.KVCache(0x1000, 0x2000, 64, base)
+    rc = lib.acespec_commit_kv(None, ctypes.byref(kv), 0x3000, 0x4000, None, B, N, base + 16,
+                               None)
+    assert rc == A.ACESPEC_EINVAL and "ctx is NULL" in A.acespec_last_error()

@@ -23,34 +23,30 @@ def small_bf16(**kw):
     return synth.Workload(**base)
 
 
-def _logits_rows(run, z_ref):
-    """GPU logits of the sampled sessions, row-indexed like the outputs."""
-    n1 = run.host_in["tokens"].shape[1]
-    zg = run.outs["logits_out"]
-    rows = {}
-    for i, b in enumerate(run.sessions):
-        for r in range(n1):
-            rows[b * n1 + r] = zg[b * n1 + r].numpy().astype(np.float64)
-    return rows
-
-
 def _check_tree(run, tol):
+    """Logits of the forward-sampled sessions against the oracle's float64 forward;
+    decisions of EVERY row of every session against the oracle's verify stage on the GPU's
+    logits; the walk of every session from the GPU's decisions."""
     z_ref = hz.oracle_tree_logits(run)
     n1 = run.host_in["tokens"].shape[1]
     zg = np.stack([run.outs["logits_out"][b * n1:(b + 1) * n1].numpy() for b in run.sessions])
     err = hz.logits_rel_err(zg.astype(np.float64), z_ref)
-    hz.log(f"logits max rel err {err.max():.3e} (tol {tol})")
+    hz.log(f"logits max rel err {err.max():.3e} over {len(run.sessions)} sessions (tol {tol})")
     assert err.max() <= tol, err.max()
-    rep = hz.check_tree_decisions(run, _logits_rows(run, z_ref))
-    hz.log(f"decisions: {rep}")
+    rep = hz.check_tree_decisions(run)
+    hz.log(f"decisions (all {run.host_in['tokens'].shape[0]} sessions): {rep}")
+    info = hz.agreement_on_oracle_logits(run, z_ref)
+    hz.log(f"informational, on the oracle's own logits: {info}")
     assert rep.ok(), str(rep)
     return err, rep
 
 
-def test_tree_tiny_fp32_full_config():
-    """The tiny fp32 workload at its full size (2 layers, d=256, vocab 4096, 8-node tree)."""
+@pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("tiny-fp32"), 10))
+def test_tree_tiny_fp32_full_config(seed):
+    """The tiny fp32 workload at its full size (2 layers, d=256, vocab 4096, 8-node tree),
+    ten parity seeds."""
     w = synth.get("tiny-fp32")
-    run = hz.run_tree(w)
+    run = hz.run_tree(w, seed=seed)
     _check_tree(run, tol=1e-4)
 
 
@@ -59,6 +55,9 @@ def test_tree_tiny_fp32_full_config():
     dict(hd=128, H=4, Hkv=1, d=256, tree="chain_sib", depth=6, sib=2, V=4100),
     dict(hd=128, H=8, Hkv=8, tree="chain", depth=9, B=2, S=64, ragged=False, V=2048),
     dict(hd=64, H=8, Hkv=2, tree="chain_sib", depth=8, sib=7, B=2, S=700, top_k=64),
+    # 8 query heads per kv head under a 64-node tree: 520 query rows, two query groups
+    dict(hd=64, H=16, Hkv=2, d=256, tree="chain_sib", depth=8, sib=7, B=2, S=300, top_k=32),
+    dict(hd=128, H=8, Hkv=1, d=256, tree="chain_sib", depth=8, sib=7, B=3, S=200, V=3000),
 ])
 def test_tree_small_bf16(variant):
     w = small_bf16(**variant)
@@ -74,32 +73,44 @@ def test_tree_empty_tree_and_long_ragged_prefix():
     assert run.outs["path_len"].tolist() == [0] * 5
 
 
-def test_tree_1b_full_size_sampled_sessions():
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("1b-bf16"), 4))
+def test_tree_1b_full_size(seed):
+    """1B-class workload at full size, all 16 sessions through the oracle's forward."""
     w = synth.get("1b-bf16")
-    run = hz.run_tree(w, sessions=[0, 9, 15])
+    run = hz.run_tree(w, seed=seed)
     _check_tree(run, tol=2e-2)
 
 
 @pytest.mark.timeout(900)
-def test_tree_8b_full_size_sampled_session():
+@pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("8b-bf16"), 3))
+def test_tree_8b_full_size(seed):
+    """8B-class workload at full size: the oracle's forward on 4 sessions spread over the
+    batch, decisions on all 64 sessions' 1088 rows."""
     w = synth.get("8b-bf16")
-    run = hz.run_tree(w, sessions=[37])
+    i = (seed - w.seed_base) // 100
+    run = hz.run_tree(w, seed=seed, sessions=[5 + i, 21 + i, 37 + i, 63 - i])
     _check_tree(run, tol=2e-2)
 
 
 @pytest.mark.timeout(900)
-def test_tree_8b_geometric_tree_sampled_session():
+def test_tree_8b_geometric_tree():
     """A paper-shaped tree: main chain of 8 with 24 alternatives allocated by the geometric
     decay of Section IV (32 drafted nodes per session)."""
     w = synth.get("8b-geometric")
-    run = hz.run_tree(w, sessions=[23])
+    run = hz.run_tree(w, sessions=[0, 23])
     _check_tree(run, tol=2e-2)
 
 
 @pytest.mark.timeout(900)
-def test_tree_8b_long_wide_sampled_session():
+@pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("8b-long-wide"), 3))
+def test_tree_8b_long_wide(seed):
+    """Long-context wide-tree workload at full size (16k-token prefixes, 64-node trees):
+    the first seed runs the oracle's forward on all 8 sessions, the others on two."""
     w = synth.get("8b-long-wide")
-    run = hz.run_tree(w, sessions=[5])
+    i = (seed - w.seed_base) // 100
+    sessions = list(range(8)) if i == 0 else [2 * i, 7 - i]
+    run = hz.run_tree(w, seed=seed, sessions=sessions)
     _check_tree(run, tol=2e-2)
 
 
@@ -111,7 +122,17 @@ def test_tree_paper_scale_widths(name):
     runs the launch configuration of the full-depth model (depth changes only the layer
     loop), and the float64 oracle stays within seconds per session."""
     w = synth.get(name).scaled(L=2)
-    run = hz.run_tree(w, sessions=[11])
+    run = hz.run_tree(w, sessions=[11, 50])
+    _check_tree(run, tol=2e-2)
+
+
+@pytest.mark.timeout(900)
+def test_tree_70b_widths_64_node_tree():
+    """The 70B-class widths (8 query heads per kv head) under the long-context workload's
+    64-node tree: 520 query rows per kv head, more than one attention workgroup holds."""
+    w = synth.get("70b-bf16").scaled(L=2, B=4, S=1024, tree="chain_sib", depth=8, sib=7,
+                                     top_k=64, T=1.0, q_T=1.0, name="70b-wide")
+    run = hz.run_tree(w, sessions=[1, 3])
     _check_tree(run, tol=2e-2)
 
 
@@ -120,16 +141,20 @@ def test_tree_paper_scale_widths(name):
 # ---------------------------------------------------------------------------------------
 
 
-def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False):
+def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False, seed=None):
+    """LM-head tail through the C ABI: logits of rows_check (default all) against the
+    oracle's float64 LM head; decisions of EVERY row against the oracle's verify stage on
+    the GPU's logits; the chain walk from the GPU's accept bits."""
     from paper_2609_02514_amd.acespec import Verifier
     dev = "cuda"
-    W = W or synth.make_weights(w, dev)
-    batch = synth.make_batch(w, dev, weights=W)
+    seed = w.seed_base if seed is None else seed
+    W = W or synth.make_weights(w, dev, seed)
+    batch = synth.make_batch(w, dev, seed, weights=W)
     R = w.rows
     q_h, u_h, d_h = hz.host(batch.q), hz.host(batch.u), hz.host(batch.draft_tokens)
     v = Verifier.for_workload(w)
     outs = v.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, dev, True)
-    hz.log(f"verify_tail R={R} V={w.V}")
+    hz.log(f"verify_tail R={R} V={w.V} seed={seed}")
     v.verify_tail(W.lm_head, W.final_norm if final_norm else None, batch.hidden,
                   batch.draft_tokens, batch.q, batch.u, w.chain_len, w.T, w.top_p, w.top_k, outs)
     torch.cuda.synchronize()
@@ -137,20 +162,17 @@ def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False):
     v.close()
     rows = list(range(R)) if rows_check is None else rows_check
     z_ref = om.lm_head_tail(W, batch.hidden[rows], final_norm=final_norm, eps=w.rms_eps)
-    zg = g["logits_out"][rows].numpy().astype(np.float64)
-    err = hz.logits_rel_err(zg, z_ref)
-    hz.log(f"tail logits max rel err {err.max():.3e}")
+    zg = g["logits_out"].numpy()
+    err = hz.logits_rel_err(zg[rows].astype(np.float64), z_ref)
+    hz.log(f"tail logits max rel err {err.max():.3e} over {len(rows)} rows")
     assert err.max() <= tol
-    rep = hz.Report()
-    for i, r in enumerate(rows):
-        z = zg[i]
-        qr = q_h[r].numpy().astype(np.float64)
-        u = u_h[r].numpy().astype(np.float64)
-        hz.compare_row_decisions(rep, f"r{r}", z, qr, [r], None, u, w.T, w.top_p, w.top_k, g, r,
-                                 {})
-        hz.compare_child(rep, f"c{r}", z, qr, int(d_h[r]), float(u[0]), float(u[1]), w.T,
-                         w.top_p, int(g["accept"][r]), int(g["resample_token"][r]))
-    hz.log(f"tail decisions: {rep}")
+    gn = {k: (t.numpy() if t is not None else None) for k, t in g.items()}
+    rep = hz.check_rows(hz.tail_jobs(zg, q_h.numpy(), d_h.numpy(), u_h.numpy(), range(R),
+                                     z_row_of=lambda r: r), gn, w.T, w.top_p, w.top_k)
+    hz.log(f"tail decisions (all {R} rows): {rep}")
+    info = hz.check_rows(hz.tail_jobs(z_ref, q_h.numpy(), d_h.numpy(), u_h.numpy(), rows),
+                         gn, w.T, w.top_p, w.top_k)
+    hz.log(f"informational, on the oracle's own logits ({len(rows)} rows): {info}")
     assert rep.ok(), str(rep)
     # chain walk from the GPU's own accept bits
     pl, nx = ov.walk_tail(g["accept"].numpy(), g["resample_token"].numpy(), w.chain_len)
@@ -212,11 +234,14 @@ def test_tail_parameter_extremes(T, top_p, top_k):
 
 
 @pytest.mark.timeout(900)
-def test_tail_8b_full_size_sampled_rows():
+@pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("8b-lmhead-tail"), 3))
+def test_tail_8b_full_size(seed):
+    """The LM-head tail at full size (4096 rows, vocab 128256): decisions on all rows,
+    the float64 LM head on 512 sampled rows."""
     w = synth.get("8b-lmhead-tail")
-    rng = np.random.default_rng(0)
-    rows = sorted(rng.choice(w.rows, 48, replace=False).tolist())
-    g = _run_tail(w, rows_check=rows, tol=1e-4)
+    rng = np.random.default_rng(seed)
+    rows = sorted(rng.choice(w.rows, 512, replace=False).tolist())
+    g = _run_tail(w, rows_check=rows, tol=1e-4, seed=seed)
     rate = float(g["accept"].float().mean())
     hz.log(f"tail acceptance rate {rate:.3f}")
     assert 0.3 < rate < 0.95

@@ -195,6 +195,22 @@ def test_top_p_hand_vectors():
     np.testing.assert_allclose(p, g["expect_p"], atol=1e-15)
 
 
+def test_temperature_hand_vectors():
+    """The logits are divided by T before the softmax (Section III-B): at T = 1/2 the
+    tempered distribution is the square of the untempered one renormalised, at T = 2 its
+    square root; the nucleus and the top-k payload follow from the tempered values."""
+    g = GOLD["temperature"]
+    z = np.array(g["z"])
+    for c in g["cases"]:
+        pt = ov.tempered_softmax(z, c["T"])
+        np.testing.assert_allclose(pt, c["expect_p_tilde"], rtol=1e-12)
+        p, order, m = ov.nucleus(pt, c["top_p"])
+        np.testing.assert_allclose(p, c["expect_p"], rtol=1e-12, atol=1e-15)
+        ids, probs = ov.topk_payload(p, order, 2)
+        assert ids.tolist() == [0, 1]
+        np.testing.assert_allclose(probs, np.array(c["expect_p"])[:2], rtol=1e-12)
+
+
 def test_accept_residual_hand_vector():
     g = GOLD["accept_residual"]
     p, q = np.array(g["p"]), np.array(g["q"])
