@@ -194,6 +194,27 @@ int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final
                         const acespec_params *params, const acespec_outputs *outs,
                         hipStream_t stream);
 
+/* acespec_verify_tail without a context, for callers that cannot allocate device memory
+ * at all (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results as acespec_verify_tail, the intermediate data
+ * in a fixed device array of the library (48 MiB per device, held from the first call on
+ * that device until the process ends).  Nothing is allocated, by this call or at set-up.
+ *  desc: the model (only dtype, d_model, vocab and rms_eps are read).
+ *  outs->logits_out is REQUIRED: the fp32 logits [R, vocab] are written there.
+ * R is limited by the array: R * (4 + 4 ceil(vocab / 128) + d_model * 2) bytes (d_model * 4
+ * for an fp32 model with a final norm; no d_model term for an fp32 model without one) must
+ * fit in 48 MiB, else ACESPEC_EINVAL before anything is launched (e.g. R <= 4096 at
+ * d_model 4096, vocab 128256).  The LM head is never sliced along K here.
+ * All calls on one device share the array: two calls that overlap in time on the same
+ * device race (serialise them, e.g. on one stream).  Every byte a call reads from the
+ * array it has written first, so no clearing is needed between calls. */
+int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_head,
+                                const void *final_norm, const void *hidden,
+                                const int32_t *draft_tokens, const float *draft_q,
+                                const float *uniforms, int R, int chain_len,
+                                const acespec_params *params, const acespec_outputs *outs,
+                                hipStream_t stream);
+
 /* Commits the accepted path of every session into its KV cache (Algorithm 1, the
  * cloud's COMPACT_KV after RECEIVE_WAIT: only the state of the kept prefix survives a
  * verify round).  Inputs are a verify_tree call's outputs over the same cache:

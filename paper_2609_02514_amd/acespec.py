@@ -21,7 +21,7 @@ ACESPEC_F32, ACESPEC_BF16 = 0, 1
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",
             "acespec_verify_tree_scalar_q", "acespec_verify_tail", "acespec_commit_kv",
             "acespec_last_error", "acespec_timing_enable", "acespec_timing_read",
-            "acespec_timing_only"]
+            "acespec_timing_only", "acespec_verify_tail_noalloc"]
 
 
 class ModelDesc(C.Structure):
@@ -86,6 +86,12 @@ def load(path: str = LIB_PATH) -> C.CDLL:
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int,
                                         C.POINTER(Params), C.POINTER(Outputs), C.c_void_p]
     lib.acespec_verify_tail.restype = C.c_int
+    lib.acespec_verify_tail_noalloc.argtypes = [C.POINTER(ModelDesc), C.c_void_p, C.c_void_p,
+                                                C.c_void_p, C.c_void_p, C.c_void_p,
+                                                C.c_void_p, C.c_int, C.c_int,
+                                                C.POINTER(Params), C.POINTER(Outputs),
+                                                C.c_void_p]
+    lib.acespec_verify_tail_noalloc.restype = C.c_int
     lib.acespec_commit_kv.argtypes = [C.c_void_p, C.POINTER(KVCache), C.c_void_p, C.c_void_p,
                                       C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
     lib.acespec_commit_kv.restype = C.c_int
@@ -156,6 +162,16 @@ def acespec_verify_tail(ctx, lm_head: int, final_norm: Optional[int], hidden: in
     return _check(load().acespec_verify_tail(ctx, lm_head, final_norm, hidden, draft_tokens,
                                              draft_q, uniforms, R, chain_len, C.byref(params),
                                              C.byref(outputs), stream))
+
+
+def acespec_verify_tail_noalloc(desc: ModelDesc, lm_head: int, final_norm: Optional[int],
+                                hidden: int, draft_tokens: int, draft_q: int, uniforms: int,
+                                R: int, chain_len: int, params: Params, outputs: Outputs,
+                                stream: int) -> int:
+    return _check(load().acespec_verify_tail_noalloc(C.byref(desc), lm_head, final_norm, hidden,
+                                                     draft_tokens, draft_q, uniforms, R,
+                                                     chain_len, C.byref(params),
+                                                     C.byref(outputs), stream))
 
 
 def acespec_commit_kv(ctx, kv: KVCache, path: int, path_len: int, status: Optional[int], B: int,

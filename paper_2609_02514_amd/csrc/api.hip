@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -93,7 +94,7 @@ hipEvent_t get_event(acespec_ctx *c) {
 template <typename F>
 int run(acespec_ctx *c, int kind, hipStream_t s, F &&launch) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  const bool timed = c->timing && ((c->timing_mask >> kind) & 1u);
+  const bool timed = c && c->timing && ((c->timing_mask >> kind) & 1u);
   if (timed) {
     e0 = get_event(c);
     e1 = get_event(c);
@@ -223,38 +224,49 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   return ACESPEC_OK;
 }
 
+// Where one LM-head + verify call keeps its intermediate data.
+struct TailWorkspace {
+  float *logits;      // [R, V] when the caller keeps no logits_out
+  float *tile_max;    // [R, ceil(V / 128)]
+  uint32_t *cand;     // [R, cand_cap] or NULL (the vocabulary kernel re-reads the row)
+  int cand_cap;
+  int32_t *rowflag;   // [R]
+  void *a;            // [R, d_model] activation type: normalised / widened hidden states
+  GemmAux aux;        // split-K partials (part_cap 0: the LM head is never split)
+};
+
+// ctx only times the launches (NULL: no timing).
 template <typename T>
-int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
-                     const void *hidden, const int32_t *draft, const float *draft_q,
-                     const float *uniforms, int R, int chain_len, const acespec_params *p,
-                     const acespec_outputs *o, hipStream_t stream) {
+int verify_tail_run(acespec_ctx *ctx, const acespec_model_desc &d, const TailWorkspace &ws,
+                    const void *lm_head, const void *final_norm, const void *hidden,
+                    const int32_t *draft, const float *draft_q, const float *uniforms, int R,
+                    int chain_len, const acespec_params *p, const acespec_outputs *o,
+                    hipStream_t stream) {
   typedef typename ActOf<T>::type A;
-  const acespec_model_desc &d = ctx->d;
   const int D = d.d_model, V = d.vocab;
-  float *logits = o->logits_out ? o->logits_out : ctx->logits;
-  const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus};
+  float *logits = o->logits_out ? o->logits_out : ws.logits;
   const A *h_in = (const A *)hidden;
   if (final_norm) {
-    RUN(K_RMSNORM, (launch_rmsnorm<T, T>((const T *)hidden, (const T *)final_norm, (A *)ctx->a,
+    RUN(K_RMSNORM, (launch_rmsnorm<T, T>((const T *)hidden, (const T *)final_norm, (A *)ws.a,
                                          R, D, d.rms_eps, stream)));
-    h_in = (const A *)ctx->a;
+    h_in = (const A *)ws.a;
   } else if (sizeof(T) == 2) {  // bf16 hidden states: widen to fp16 for the f16 MFMA path
-    RUN(K_RMSNORM, launch_cast_bf16_f16((const bf16 *)hidden, (f16 *)ctx->a, (size_t)R * D,
+    RUN(K_RMSNORM, launch_cast_bf16_f16((const bf16 *)hidden, (f16 *)ws.a, (size_t)R * D,
                                         stream));
-    h_in = (const A *)ctx->a;
+    h_in = (const A *)ws.a;
   }
   int ntile = 0;
   RUN(K_GEMM_LM, (launch_lm_head<T, A>(h_in, (const T *)lm_head, R, V, D, logits,
-                                       ctx->tile_max, &ntile, aux, stream)));
+                                       ws.tile_max, &ntile, ws.aux, stream)));
   VocabArgs va{};
   va.logits = logits;
   va.q = draft_q;
   va.q_scalar = nullptr;
-  va.tile_max = ntile ? ctx->tile_max : nullptr;
+  va.tile_max = ntile ? ws.tile_max : nullptr;
   va.ntile = ntile;
-  va.cand = ctx->cand;
-  va.cand_cap = kCandCap;
-  va.rowflag = ctx->rowflag;
+  va.cand = ws.cand;
+  va.cand_cap = ws.cand_cap;
+  va.rowflag = ws.rowflag;
   va.u = uniforms;
   va.tok = draft;
   va.par = nullptr;
@@ -271,10 +283,21 @@ int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_no
   va.topk_ids = o->topk_ids;
   va.topk_probs = o->topk_probs;
   RUN(K_VOCAB, launch_vocab(va, stream));
-  RUN(K_WALK, launch_walk_tail(o->accept, o->resample_token, draft, ctx->rowflag, R,
+  RUN(K_WALK, launch_walk_tail(o->accept, o->resample_token, draft, ws.rowflag, R,
                                chain_len, V, o->acc_prefix_len, o->path, o->path_len,
                                o->next_token, o->sibling_hit, o->status, stream));
   return ACESPEC_OK;
+}
+
+template <typename T>
+int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
+                     const void *hidden, const int32_t *draft, const float *draft_q,
+                     const float *uniforms, int R, int chain_len, const acespec_params *p,
+                     const acespec_outputs *o, hipStream_t stream) {
+  const TailWorkspace ws{ctx->logits, ctx->tile_max, ctx->cand, kCandCap, ctx->rowflag, ctx->a,
+                         GemmAux{ctx->gpart, ctx->gpart_cap, ctx->cus}};
+  return verify_tail_run<T>(ctx, ctx->d, ws, lm_head, final_norm, hidden, draft, draft_q,
+                            uniforms, R, chain_len, p, o, stream);
 }
 
 }  // namespace
@@ -589,6 +612,114 @@ int acespec_timing_read(acespec_ctx *ctx, const char **names, double *total_ms, 
     ctx->launches[k] = 0;
   }
   return n;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------------------------
+// Allocation-free LM-head verify (acespec_verify_tail_noalloc)
+// ------------------------------------------------------------------------------------
+// Its intermediate data lives in a file-scope device array, one copy per device, held
+// until the process ends.  On the host the array's name is not a device address: the
+// address comes from hipGetSymbolAddress, taken once per device with that device current,
+// and only that address is ever handed to kernels.  Calls on one device share the array,
+// so calls that overlap in time on one device race.
+namespace {
+
+constexpr size_t kScratchBytes = (size_t)48 << 20;
+__device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+int g_scratch_cus[kMaxDevices] = {};
+
+int scratch_of_current_device(char **ptr, int *cus) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(ACESPEC_EHIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(ACESPEC_EUNSUPPORTED, "device %d is beyond the %d the scratch table holds", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(ACESPEC_EHIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    g_scratch_ptr[dev] = (char *)p;
+    g_scratch_cus[dev] = n;
+  }
+  *ptr = g_scratch_ptr[dev];
+  *cus = g_scratch_cus[dev];
+  return ACESPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_head,
+                                const void *final_norm, const void *hidden,
+                                const int32_t *draft_tokens, const float *draft_q,
+                                const float *uniforms, int R, int chain_len,
+                                const acespec_params *p, const acespec_outputs *o,
+                                hipStream_t stream) {
+  g_err.clear();
+  if (!desc) return fail(ACESPEC_EINVAL, "desc is NULL");
+  const acespec_model_desc &d = *desc;
+  if (d.dtype != ACESPEC_F32 && d.dtype != ACESPEC_BF16)
+    return fail(ACESPEC_EINVAL, "unknown dtype %d", (int)d.dtype);
+  if (d.d_model < 64 || d.d_model % 64 || d.vocab < 1 || d.vocab % 4 || d.vocab > 262144)
+    return fail(ACESPEC_EUNSUPPORTED,
+                "need d_model a multiple of 64, vocab a multiple of 4 and <= 262144");
+  if (!lm_head || !hidden || !draft_tokens || !draft_q || !uniforms)
+    return fail(ACESPEC_EINVAL, "a required pointer is NULL");
+  if (R < 1) return fail(ACESPEC_EINVAL, "R must be >= 1 (got %d)", R);
+  if (chain_len < 1 || R % chain_len)
+    return fail(ACESPEC_EINVAL, "chain_len must be >= 1 and divide R");
+  int rc = check_params(p, d.vocab);
+  if (rc) return rc;
+  rc = check_outputs(o);
+  if (rc) return rc;
+  if (!o->logits_out)
+    return fail(ACESPEC_EINVAL, "logits_out is required here: the logits are written there");
+  // scratch layout: row flags, LM-head row maxima per 128-column tile, the hidden states
+  // in the activation type (bf16 model, or any model with a final norm), and the
+  // vocabulary kernel's candidate lists when they still fit
+  const size_t esz = d.dtype == ACESPEC_BF16 ? 2 : 4;
+  const bool need_a = d.dtype == ACESPEC_BF16 || final_norm != nullptr;
+  const size_t b_flag = align_up((size_t)R * 4);
+  const size_t b_tmax = align_up((size_t)R * ((d.vocab + 127) / 128) * 4);
+  const size_t b_a = need_a ? align_up((size_t)R * d.d_model * esz) : 0;
+  const size_t b_cand = align_up((size_t)R * kCandCap * 4);
+  const size_t need = b_flag + b_tmax + b_a;
+  if (need > kScratchBytes)
+    return fail(ACESPEC_EINVAL,
+                "R = %d rows of d_model %d and vocab %d need %zu scratch bytes; the "
+                "allocation-free entry point holds %zu (use acespec_verify_tail)",
+                R, d.d_model, d.vocab, need, kScratchBytes);
+  char *base = nullptr;
+  int cus = 256;
+  rc = scratch_of_current_device(&base, &cus);
+  if (rc) return rc;
+  const bool cand = need + b_cand <= kScratchBytes;
+  TailWorkspace ws{nullptr,
+                   (float *)(base + b_flag),
+                   cand ? (uint32_t *)(base + need) : nullptr,
+                   cand ? kCandCap : 0,
+                   (int32_t *)base,
+                   need_a ? (void *)(base + b_flag + b_tmax) : nullptr,
+                   GemmAux{nullptr, 0, cus}};
+  if (d.dtype == ACESPEC_BF16)
+    return verify_tail_run<bf16>(nullptr, d, ws, lm_head, final_norm, hidden, draft_tokens,
+                                 draft_q, uniforms, R, chain_len, p, o, stream);
+  return verify_tail_run<float>(nullptr, d, ws, lm_head, final_norm, hidden, draft_tokens,
+                                draft_q, uniforms, R, chain_len, p, o, stream);
 }
 
 }  // extern "C"

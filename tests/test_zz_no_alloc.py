@@ -1,0 +1,60 @@
+"""The allocation-free LM-head verify (acespec_verify_tail_noalloc) through the C ABI
+against acespec_verify_tail on the same inputs: every output bitwise equal, on two calls
+in a row, the second with fewer rows (the shared scratch keeps the first call's data)."""
+import pytest
+import torch
+
+import synth
+from paper_2609_02514_amd import acespec as A
+from tests import harness as hz
+
+pytestmark = pytest.mark.gpu
+
+
+def _outs(R, w):
+    return A.Verifier.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, "cuda", True)
+
+
+@pytest.mark.parametrize("final_norm", [False, True])
+def test_noalloc_tail_equals_context_tail(final_norm):
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-noalloc", rows=512, chain_len=16)
+    W = synth.make_weights(w, "cuda")
+    batch = synth.make_batch(w, "cuda", weights=W)
+    gain = (1.0 + synth.normal((w.d,), 0.1, torch.float32, "cuda", w.seed_base, 0, 2)).to(
+        torch.bfloat16) if final_norm else None
+    v = A.Verifier.for_workload(w)
+    stream = torch.cuda.current_stream().cuda_stream
+    for R in (512, 256):                  # second call: fewer rows
+        ref = _outs(R, w)
+        v.verify_tail(W.lm_head, gain, batch.hidden[:R], batch.draft_tokens[:R], batch.q[:R],
+                      batch.u[:R], w.chain_len, w.T, w.top_p, w.top_k, ref)
+        got = _outs(R, w)
+        for t in got.values():
+            if t is not None:
+                t.fill_(-7)
+        A.acespec_verify_tail_noalloc(v.desc, W.lm_head.data_ptr(),
+                                      gain.data_ptr() if gain is not None else None,
+                                      batch.hidden[:R].data_ptr(),
+                                      batch.draft_tokens[:R].data_ptr(), batch.q[:R].data_ptr(),
+                                      batch.u[:R].data_ptr(), R, w.chain_len,
+                                      A.Params(w.T, w.top_p, w.top_k),
+                                      A.Verifier.outputs_struct(got), stream)
+        torch.cuda.synchronize()
+        for k, t in ref.items():
+            if t is not None:
+                assert torch.equal(t, got[k]), (R, k)
+        assert got["status"].tolist() == [0] * (R // w.chain_len)
+        hz.log(f"no-alloc tail R={R} final_norm={final_norm}: every output equals verify_tail")
+    v.close()
+
+
+def test_noalloc_rejects_rows_beyond_its_scratch():
+    w = synth.get("8b-lmhead-tail")
+    desc = A.ModelDesc(0, w.d, 0, 1, 0, 0, w.V, 10000.0, 1e-5, A.ACESPEC_BF16)
+    R = 8192
+    fake = A.Outputs(*([0x1000] * 12))
+    with pytest.raises(A.AcespecError) as e:
+        A.acespec_verify_tail_noalloc(desc, 0x1000, None, 0x1000, 0x1000, 0x1000, 0x1000, R, 16,
+                                      A.Params(0.6, 0.8, 8), fake,
+                                      torch.cuda.current_stream().cuda_stream)
+    assert e.value.code == A.ACESPEC_EINVAL and "scratch" in str(e.value)
