@@ -56,7 +56,9 @@ def build(verbose=True):
     if verbose:
         print(f"built {LIB}")
     tmp = CALIB_LIB + ".tmp"
-    cmd = [HIPCC] + FLAGS + ["-shared", CALIB_SRC, "-o", tmp]
+    # accumulators in VGPRs: the AGPR form of the MFMA loop copies accumulators each pass
+    cmd = [HIPCC] + FLAGS + ["-mllvm", "-amdgpu-mfma-vgpr-form=1", "-shared", CALIB_SRC,
+                             "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("calibration library build failed:\n" + r.stdout + r.stderr)

@@ -58,9 +58,12 @@ AS_DEVICE int xcd_tile(int bid, int total) {
 //   free stage; next-stage fragments are always read) so the compiler counts
 //   outstanding LDS reads exactly, and fragment reads are fenced against the MFMAs.
 // ------------------------------------------------------------------------------------
-// Byte offset of 16-byte piece `pc` of row `row` in rows of ROWB bytes.
+// Byte offset of 16-byte piece `pc` of row `row` in rows of ROWB bytes.  The piece index
+// is XORed with (row / 2): measured on gfx950, a 16-lane fragment read (16 rows, one
+// logical piece each) then runs at the LDS's full rate for 64- and 128-byte rows alike,
+// where XORing with the row's 256-byte bank round (row / 4 for 64-byte rows) halves it.
 template <int ROWB> AS_DEVICE int piece_off(int row, int pc) {
-  const int sw = (row / (256 / ROWB)) & (ROWB / 16 - 1);
+  const int sw = (row >> 1) & (ROWB / 16 - 1);
   return row * ROWB + ((pc ^ sw) << 4);
 }
 
