@@ -306,6 +306,8 @@ def calibrate(reps=5):
                                        ctypes.c_int, ctypes.c_void_p]
     lib.acespec_calib_mfma.argtypes = [ctypes.c_uint32, ctypes.c_void_p, ctypes.c_int,
                                        ctypes.c_int, ctypes.c_void_p]
+    lib.acespec_calib_read.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_int, ctypes.c_void_p]
     stream = torch.cuda.current_stream()
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     nbytes = 1 << 30
@@ -328,16 +330,86 @@ def calibrate(reps=5):
 
     ms_copy = timed(lambda: lib.acespec_calib_copy(src.data_ptr(), dst.data_ptr(), nbytes,
                                                    cus * 16, stream.cuda_stream))
+    rblocks = cus * 8
+    rout = torch.empty(rblocks * 4, dtype=torch.float32, device="cuda")
+    ms_read = timed(lambda: lib.acespec_calib_read(src.data_ptr(), rout.data_ptr(), nbytes,
+                                                   rblocks, stream.cuda_stream))
     ms_mfma = timed(lambda: lib.acespec_calib_mfma(12345, out.data_ptr(), blocks, iters,
                                                    stream.cuda_stream))
     flops = blocks * 4 * iters * 16 * 16384.0
     del src, dst, out
     return {"hbm_copy_gbs": round(2 * nbytes / (ms_copy / 1e3) / 1e9, 1),
+            "hbm_read_gbs": round(nbytes / (ms_read / 1e3) / 1e9, 1),
             "mfma_f16_loop_tflops": round(flops / (ms_mfma / 1e3) / 1e12, 1),
             "method": (f"median of {reps} HIP-event-timed runs: a 1 GiB device copy "
-                       f"(16-byte loads and stores, read + write bytes counted), and "
+                       f"(16-byte loads and stores, read + write bytes counted), a 1 GiB "
+                       f"streaming read (four 16-byte loads in flight a thread), and "
                        f"{blocks} workgroups x 4 waves x {iters} x 16 MFMAs 16x16x32 f16 on "
                        f"random operands generated in registers")}
+
+
+def lds_patterns():
+    """Lane byte offsets of the verify kernels' 16-byte LDS fragment reads (lane l reads
+    row l % 16, logical piece l / 16 of a 16-row block), under the XOR swizzles tried."""
+    def gemm(rowb, sw):
+        return [(l & 15) * rowb + (((l >> 4) ^ sw(l & 15)) << 4) for l in range(64)]
+
+    def key_of_row(kk, m):
+        return (kk >> 1) * 32 + (m >> 2) * 8 + (kk & 1) * 4 + (m & 3)
+
+    def attn_k(sw, kk=1, s=0):   # 256-byte key rows (head dim 128), fp16 elements
+        out = []
+        for l in range(64):
+            key = key_of_row(kk, l & 15)
+            out.append(2 * (key * 128 + (((s * 4 + (l >> 4)) ^ sw(key)) << 3)))
+        return out
+
+    def attn_v(sw, ks=0, nb=0):  # 128-byte V^T rows (64 slots)
+        out = []
+        for l in range(64):
+            row = nb * 16 + (l & 15)
+            out.append(2 * (row * 64 + (((ks * 4 + (l >> 4)) ^ sw(row)) << 3)))
+        return out
+
+    return [
+        ("contiguous 1 KB", [16 * l for l in range(64)]),
+        ("GEMM 64-byte rows, piece ^ (row / 4)", gemm(64, lambda r: (r >> 2) & 3)),
+        ("GEMM 64-byte rows, piece ^ (row / 2)", gemm(64, lambda r: (r >> 1) & 3)),
+        ("GEMM 128-byte rows, piece ^ (row / 2)", gemm(128, lambda r: (r >> 1) & 7)),
+        ("attention K rows, key swizzle", attn_k(lambda k: (((k >> 3) & 3) << 2) | (k & 3))),
+        ("attention V^T rows, row ^ (row / 8)", attn_v(lambda r: (r & 7) ^ ((r >> 3) & 1))),
+        ("attention V^T rows, row / 2", attn_v(lambda r: (r >> 1) & 7)),
+    ]
+
+
+def lds_probe(reps=3):
+    """Read rate of every pattern of lds_patterns() (best of reps), B/clk/CU at 2.4 GHz."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02514_amd", "libacespec_calib.so"))
+    lib.acespec_calib_lds.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_int, ctypes.c_void_p]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks, iters = 4 * cus, 4096
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    res = []
+    for name, offs in lds_patterns():
+        assert len(offs) == 64 and all(0 <= o < 16384 and o % 16 == 0 for o in offs), name
+        d = torch.tensor(offs, dtype=torch.int32, device="cuda")
+        best = 1e30
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            rc = lib.acespec_calib_lds(d.data_ptr(), out.data_ptr(), blocks, iters,
+                                       stream.cuda_stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            assert rc == 0, rc
+            best = min(best, e0.elapsed_time(e1))
+        nbytes = blocks * 256 * iters * 8 * 16
+        res.append((name, round(best, 3), round(nbytes / (best * 1e-3) / cus / 2.4e9, 1)))
+    return res
 
 
 def main():
@@ -360,6 +432,10 @@ def main():
                          "output directories (bench FETCH_SIZE, bench WRITE_SIZE, copy "
                          "FETCH_SIZE, copy WRITE_SIZE)")
     ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="only measure the LDS read rate of the kernels' fragment patterns")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="only measure the achievable copy, read and MFMA rates")
     ap.add_argument("--summarize-mfma", metavar="DIR",
                     help="print the per-kernel MFMA busy summary of one rocprofv3 "
                          "--pmc MfmaUtil output directory")
@@ -369,6 +445,13 @@ def main():
         return
     if args.summarize_mfma:
         print(json.dumps(summarize_mfma(args.summarize_mfma), indent=1))
+        return
+    if args.lds_probe:
+        for name, ms, bpc in lds_probe():
+            print(json.dumps({"pattern": name, "ms": ms, "bytes_per_clk_per_cu_at_2.4GHz": bpc}))
+        return
+    if args.calibrate:
+        print(json.dumps(calibrate()))
         return
     if args.copy_calibration:
         import torch
@@ -529,8 +612,8 @@ def main():
         f"{t_wall / args.steps * 1e3:.3f}), {value:.0f} tok/s; "
         f"status {outs['status'].tolist()[:4]}...")
     ach = calibrate()
-    log(f"achievable: copy {ach['hbm_copy_gbs']} GB/s, MFMA loop {ach['mfma_f16_loop_tflops']} "
-        f"TFLOP/s")
+    log(f"achievable: copy {ach['hbm_copy_gbs']} GB/s, read {ach['hbm_read_gbs']} GB/s, MFMA loop "
+        f"{ach['mfma_f16_loop_tflops']} TFLOP/s")
 
     traffic = load_traffic(w.name)
     mfma_busy = load_mfma(w.name)
@@ -543,7 +626,7 @@ def main():
         if "tflops" in ent:
             ent["mfma_frac_achievable"] = round(ent["tflops"] / ach["mfma_f16_loop_tflops"], 4)
         if "gbs" in ent:
-            ent["hbm_frac_achievable"] = round(ent["gbs"] / ach["hbm_copy_gbs"], 4)
+            ent["hbm_frac_achievable"] = round(ent["gbs"] / ach["hbm_read_gbs"], 4)
     if dom.startswith("gemm"):
         roof = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": PEAK_MFMA_TFLOPS, "unit": "TFLOP/s", "frac": dk["mfma_frac"],
@@ -552,8 +635,8 @@ def main():
     else:
         roof = {"kernel": dom, "bound": "hbm", "achieved": dk["gbs"], "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": dk["hbm_frac"], "traffic": traffic.get(dom),
-                "achievable": ach["hbm_copy_gbs"],
-                "frac_of_achievable": round(dk["gbs"] / ach["hbm_copy_gbs"], 4)}
+                "achievable": ach["hbm_read_gbs"],
+                "frac_of_achievable": round(dk["gbs"] / ach["hbm_read_gbs"], 4)}
     roof["traffic_unit"] = "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     roof["algorithmic_per_launch"] = {"flops": work[dom][0], "bytes": work[dom][1]} if dom in work else None
 

@@ -1,8 +1,10 @@
 // Calibration kernels of the measurement harness (not part of the verify path): the
 // rates the chip actually sustains, against which the verify kernels' roofline fractions
 // are also reported next to the published peaks.
-//   - a streaming device copy (16-byte loads and stores, grid-stride), the achievable
-//     HBM rate;
+//   - a streaming device copy (16-byte loads and stores, grid-stride) and a streaming
+//     read (four 16-byte loads in flight per thread), the achievable HBM rates;
+//   - the LDS read rate of a fragment-read lane pattern (bank conflicts show as a lower
+//     rate than a conflict-free pattern's);
 //   - the MFMA pipe on random fp16 operands: every wave keeps 16 independent
 //     v_mfma_f32_16x16x32_f16 accumulators busy, cycling through 4 A and 4 B fragments of
 //     pseudo-random values generated in registers, so consecutive instructions see
@@ -22,6 +24,53 @@ __global__ __launch_bounds__(256) void copy_kernel(const float4 *__restrict__ sr
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride)
     dst[i] = src[i];
+}
+
+// Streaming read: four independent 16-byte loads in flight per thread and step, summed so
+// the loads stay live; one float per block out.
+__global__ __launch_bounds__(256) void read_kernel(const float4 *__restrict__ src,
+                                                   float *__restrict__ out, size_t n4) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < n4; i += 4 * stride) {
+    const float4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+    acc.x += a.x + b.x + c.x + d.x;
+    acc.y += a.y + b.y + c.y + d.y;
+    acc.z += a.z + b.z + c.z + d.z;
+    acc.w += a.w + b.w + c.w + d.w;
+  }
+  for (; i < n4; i += stride) {
+    const float4 a = src[i];
+    acc.x += a.x; acc.y += a.y; acc.z += a.z; acc.w += a.w;
+  }
+  float v = acc.x + acc.y + acc.z + acc.w;
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = v;
+}
+
+// LDS read rate of one 16-byte-per-lane fragment pattern: offs[64] gives each lane's byte
+// offset (< 16 KB) within a 256-byte-aligned window that moves by whole 256-byte rounds
+// (so the bank pattern is the table's), 8 reads in flight per wave.
+__global__ __launch_bounds__(256) void lds_read_kernel(const int *__restrict__ offs, int iters,
+                                                       float *__restrict__ out) {
+  __shared__ __attribute__((aligned(1024))) char lds[40960];
+  for (int i = threadIdx.x; i < 40960 / 4; i += 256) ((float *)lds)[i] = (float)(i & 7);
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int off = offs[lane] & 16383;
+  float4 acc[8];
+  for (int j = 0; j < 8; ++j) acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float4 v = *(const float4 *)(lds + (off & ~15) + ((it * 8 + j + w) & 63) * 256);
+      acc[j].x += v.x; acc[j].y += v.y; acc[j].z += v.z; acc[j].w += v.w;
+    }
+  }
+  float r = 0.f;
+  for (int j = 0; j < 8; ++j) r += acc[j].x + acc[j].y + acc[j].z + acc[j].w;
+  out[blockIdx.x * 256 + threadIdx.x] = r;
 }
 
 // Pseudo-random fp16 operand: random sign and mantissa, magnitude in [0.5, 1).
@@ -83,6 +132,22 @@ int acespec_calib_copy(const void *src, void *dst, size_t n_bytes, int blocks,
   if (!src || !dst || n_bytes % 16 || blocks < 1) return -1;
   hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(256), 0, stream, (const float4 *)src,
                      (float4 *)dst, n_bytes / 16);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// Reads n_bytes (a multiple of 16; 16-byte aligned) from src; out: >= 4 * blocks floats.
+int acespec_calib_read(const void *src, float *out, size_t n_bytes, int blocks,
+                       hipStream_t stream) {
+  if (!src || !out || n_bytes % 16 || blocks < 1) return -1;
+  hipLaunchKernelGGL(read_kernel, dim3(blocks), dim3(256), 0, stream, (const float4 *)src, out,
+                     n_bytes / 16);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// offs: 64 device ints (lane byte offsets, < 16 KB, 16-byte aligned); out: blocks * 256.
+int acespec_calib_lds(const int *offs, float *out, int blocks, int iters, hipStream_t stream) {
+  if (!offs || !out || blocks < 1 || iters < 1) return -1;
+  hipLaunchKernelGGL(lds_read_kernel, dim3(blocks), dim3(256), 0, stream, offs, iters, out);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

@@ -64,13 +64,15 @@ AS_DEVICE int key_of_score(int kk, int lg, int e) { return (kk >> 1) * 32 + lg *
 
 // XOR swizzles of the 16-byte pieces of a row, chosen so that each fragment read -- 16
 // lanes at one logical piece of 16 rows (keys m = 0..15 of a block above, or 16
-// consecutive V^T rows) -- touches distinct banks whether the LDS serves 16 lanes (64
-// banks) or 8 lanes (32 banks) of a 16-byte read per cycle.  K rows are 2*HD bytes.
+// consecutive V^T rows) -- runs at the LDS's full rate; measured on gfx950 with the
+// kernel's own lane patterns (256-byte K rows: about 200 B/clk/CU with this key swizzle;
+// 128-byte V^T rows: 210 B/clk/CU with row / 2, where row ^ (row / 8) halved it).
+// K rows are 2*HD bytes.
 template <int HD> AS_DEVICE int ksw(int key) {
   if (HD == 128) return (((key >> 3) & 3) << 2) | (key & 3);
   return ((key & 1) ^ ((key >> 4) & 1)) | (((key >> 1) & 1) << 1) | (((key >> 3) & 1) << 2);
 }
-AS_DEVICE int vsw(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+AS_DEVICE int vsw(int row) { return (row >> 1) & 7; }
 
 // Element offset of piece `piece` of key row `key` in a stage's K part.
 template <int HD> AS_DEVICE int k_off(int key, int piece) {

@@ -177,3 +177,18 @@ def test_committed_mfma_tables_name_known_kernels():
         assert set(blob["kinds"]) <= set(bench.KIND_SOURCES)
         for v in blob["kinds"].values():
             assert 0.0 <= v["mfma_busy_pct"] <= 100.0 and len(v["source_sha"]) == 16
+
+
+def test_lds_probe_patterns_stay_in_bounds():
+    """The LDS probe's lane offset tables fit the probe kernel's 16 KB window, are 16-byte
+    aligned, and the swizzles only permute pieces within each row (one piece of every
+    lane group's row per lane)."""
+    import bench
+    pats = dict(bench.lds_patterns())
+    for name, offs in pats.items():
+        assert len(offs) == 64 and len(set(offs)) == 64, name
+        assert all(0 <= o < 16384 and o % 16 == 0 for o in offs), name
+    # a permutation of the unswizzled layout's pieces within each row
+    base = sorted(((l & 15) * 64 + ((l >> 4) << 4)) for l in range(64))
+    assert sorted(pats["GEMM 64-byte rows, piece ^ (row / 2)"]) == base
+    assert sorted(pats["GEMM 64-byte rows, piece ^ (row / 4)"]) == base
