@@ -89,7 +89,10 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
 
   // Units: `full` whole tiles, then tsplit k-slices of each remaining tile (their partial
   // sums go to `part`, summed by tile_fixup_kernel).  Each group is dealt over the XCDs on
-  // its own (full is a multiple of 8), so the slices spread over the whole chip.
+  // its own (full is a multiple of 8), so the slices spread over the whole chip.  Slices
+  // are numbered k-slice first: an XCD's run of units then covers one k-slice (two at a
+  // boundary) of a band of weight panels, so it fetches its k-columns of the activations
+  // once for all its panels, instead of the whole activation matrix once per XCD.
   const int tiles = mt * nt;
   int tile, sp, ns;
   if ((int)blockIdx.x < full) {
@@ -97,9 +100,10 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     sp = 0;
     ns = 1;
   } else {
-    const int u = xcd_tile(blockIdx.x - full, (tiles - full) * tsplit);
-    tile = full + u / tsplit;
-    sp = u - (tile - full) * tsplit;
+    const int ntl = tiles - full;
+    const int u = xcd_tile(blockIdx.x - full, ntl * tsplit);
+    sp = u / ntl;
+    tile = full + (u - sp * ntl);
     ns = tsplit;
   }
   const int tn = tile / mt, tm = tile - tn * mt;

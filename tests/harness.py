@@ -141,16 +141,22 @@ class Report:
         self.nodes += other.nodes
         self.mismatches += other.mismatches
 
+    @property
+    def nodes_differing(self) -> int:
+        """Nodes (a row, or a drafted child) with at least one differing decision."""
+        return len({m.tag for m in self.mismatches})
+
     def ok(self, rate=RATE) -> bool:
-        return not self.unexplained and len(self.mismatches) <= int(rate * self.nodes)
+        return not self.unexplained and self.nodes_differing <= int(rate * self.nodes)
 
     def classes(self) -> Dict[str, int]:
         return dict(Counter(m.cls for m in self.mismatches))
 
     def __str__(self):
-        agree = 1.0 - len(self.mismatches) / max(1, self.nodes)
-        return (f"nodes={self.nodes} mismatches={len(self.mismatches)} "
-                f"({100 * agree:.3f} % identical) by class {self.classes()} "
+        agree = 1.0 - self.nodes_differing / max(1, self.nodes)
+        return (f"nodes={self.nodes} differing={self.nodes_differing} "
+                f"({100 * agree:.3f} % identical) mismatches={len(self.mismatches)} "
+                f"by class {self.classes()} "
                 f"first={[f'{m.tag}: {m.what} [{m.cls}]' for m in self.mismatches[:6]]}")
 
 
