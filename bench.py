@@ -83,7 +83,7 @@ def _label_dispatches(rows):
     for i, r in enumerate(rows):
         n = r["Kernel_Name"]
         kind = None
-        if "tree_attn_mfma_kernel" in n:
+        if "tree_attn_mfma_kernel" in n or "tree_attn_t32_kernel" in n:
             kind = "tree_attention"
         elif "attn_combine_kernel" in n or "tile_fixup_kernel" in n or \
                 "fixup_resid_norm_kernel" in n or "rope_kv_kernel" in n:

@@ -44,6 +44,25 @@
 namespace {
 
 constexpr int KC = 64;            // slots per chunk
+// Opens the tree-mask branch of a chunk loop: an empty volatile asm cannot be executed
+// speculatively, so the mask stays a branch taken only by the chunks that hold tree
+// slots instead of being if-converted into selects that every chunk pays for.
+#define MASK_BRANCH() __asm__ volatile("")
+
+// The chunk barrier: this wave's LDS accesses (the widening's stores, the fragment reads)
+// complete, then every wave of the workgroup arrives.  The DMA is not waited for here:
+// each stage's DMA is waited for explicitly, NST - 2 chunks ahead.  (Written out rather
+// than as an LDS release fence, with which the compiler drains every outstanding load,
+// the DMA of the chunks in flight included, at every barrier of some of these kernels.)
+// Online softmax with a lazy reference: the exponent's reference m moves to a new block
+// maximum only when that maximum exceeds m by more than LAZY_LOG2 in base 2 (or m is
+// unset), so the accumulators are rescaled a few times per query instead of at most
+// blocks; the probabilities stay below 2^LAZY_LOG2, far inside fp16, and o / l is
+// unchanged because numerator and denominator share the reference.
+constexpr float LAZY_LOG2 = 8.f;
+AS_DEVICE float lazy_ref(float m, float mx, float lazy) { return mx > m + lazy ? mx : m; }
+
+AS_DEVICE void chunk_barrier() { __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 constexpr float LOG2E = 1.4426950408889634f;
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
@@ -73,6 +92,19 @@ template <int HD> AS_DEVICE int ksw(int key) {
   return ((key & 1) ^ ((key >> 4) & 1)) | (((key >> 1) & 1) << 1) | (((key >> 3) & 1) << 2);
 }
 AS_DEVICE int vsw(int row) { return (row >> 1) & 7; }
+// K swizzle of the 32-row-tile kernel: its 16-lane fragment groups read 16 consecutive
+// keys (bits 0-3 vary) in the main tiles and keys with bits 0, 1, 3, 4 varying in the
+// remainder tile's quarter units; the XOR value below takes 16 (head_dim 128: 256-byte
+// rows, one bank round each) or 2 x 8 (head_dim 64: rows alternate between the two
+// halves of a bank round) distinct values on both sets.
+template <int HD> AS_DEVICE int ksw32(int key) {
+  const int b24 = ((key >> 2) ^ (key >> 4)) & 1;
+  if (HD == 128) return (key & 0xB) | (b24 << 2);
+  return ((key >> 1) & 1) | (b24 << 1) | (((key >> 3) & 1) << 2);
+}
+template <int HD, bool T32> AS_DEVICE int kswz(int key) {
+  return T32 ? ksw32<HD>(key) : ksw<HD>(key);
+}
 
 // Element offset of piece `piece` of key row `key` in a stage's K part.
 template <int HD> AS_DEVICE int k_off(int key, int piece) {
@@ -84,7 +116,7 @@ AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ vsw(row)) 
 
 // DMA of one chunk (keys key0 .. key0 + 63) into a stage: HD/8 blocks of 1 KB for K and
 // as many for V^T, dealt to the NW waves in turn.
-template <int HD, int NW>
+template <int HD, int NW, bool T32 = false>
 AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int key0,
                            int capacity, int wave, int lane) {
   constexpr int BLOCKS = HD / 8;
@@ -95,7 +127,7 @@ AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int 
     if (blk < BLOCKS) {
       const int e = blk * 512 + lane * 8;          // element offset this lane's bytes land at
       const int key = e / HD, piece = (e % HD) >> 3;
-      dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ ksw<HD>(key)) << 3),
+      dma16(kb + (size_t)(key0 + key) * HD + ((piece ^ kswz<HD, T32>(key)) << 3),
             (lds_ptr_t)(stage + blk * 512));
     } else {
       const int i = blk - BLOCKS;
@@ -168,6 +200,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   const size_t row0 = (size_t)b * n1;
   const int q_stride = H * HD;
   const float sscale = LOG2E / sqrtf((float)HD);   // scores -> base-2 exponent
+  const float lazy = LAZY_LOG2 / sscale;           // reference threshold in score units
 
   // Query tile t of this wave: wave + NW t.  Per tile: query fragments (B operand of
   // S^T = K Q^T), ancestor mask, running softmax state.
@@ -232,7 +265,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     if (c + 1 < c1) {
       if (c + NST - 2 < c1) wait_vmcnt<(NST - 3) * L_DMA>(); else wait_vmcnt<0>();
     }
-    lds_barrier();
+    chunk_barrier();
     if (c + NST - 1 < c1)
       issue_chunk<HD, NW>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity, wave, lane);
     if (c + 1 < c1 && widener) widen_chunk<HD>(stage_of(c + 1), wt, wstride, (c + 1) * KC, total);
@@ -258,6 +291,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
           sc[kk] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[t][s], sc[kk], 0, 0, 0);
         }
       if (tree_chunk) {
+        MASK_BRANCH();
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
@@ -275,7 +309,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) mx = fmaxf(mx, sc[kk][e]);
       mx = rows4_max(mx);
-      const float m_new = fmaxf(m_run[t], mx);
+      const float m_new = lazy_ref(m_run[t], mx, lazy);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       // raw v_exp_f32: results below 2^-126 flush to zero, which a softmax weight can spare
       const float alpha = __builtin_amdgcn_exp2f((m_run[t] - m_use) * sscale);
@@ -316,6 +350,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
         sq = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qf[QS][s], sq, 0, 0, 0);
       }
       if (tree_chunk) {
+        MASK_BRANCH();
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int j = key0 + key_of_score(qk, lg, e) - S;
@@ -326,7 +361,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
       }
       float mx = fmaxf(fmaxf(sq[0], sq[1]), fmaxf(sq[2], sq[3]));
       mx = rows4_max(mx);
-      const float m_new = fmaxf(m_run[QS], mx);
+      const float m_new = lazy_ref(m_run[QS], mx, lazy);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
       const float alpha = __builtin_amdgcn_exp2f((m_run[QS] - m_use) * sscale);
       m_run[QS] = m_new;
@@ -455,6 +490,393 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   }
 }
 
+// ------------------------------------------------------------------------------------
+// 32-row query tiles, for kv heads whose query rows exceed 16 tiles of 16 (a 64-node tree
+// under 4 or more query heads per kv head).  Eight waves, one 32-row tile each, on
+// v_mfma_f32_32x32x16_f16: every 16-byte K or V^T fragment read now feeds 32 queries
+// instead of 16, which halves the LDS fragment traffic per query, and each wave's chains
+// are twice as long.  A remainder of at most 16 rows is one 16-row tile split into four
+// quarter units (one 16-key block of every chunk each) on waves 4-7, which share SIMDs
+// with waves 0-3, merged through LDS at the end.  At most 8 x 32 + 16 rows per workgroup;
+// more rows are dealt to query groups of equal size.
+//  * S^T = K Q^T per 32-key block: A row r holds key p32(r) of the block, B holds the 32
+//    queries, so a lane holds 16 scores of one query (lane % 32) for keys
+//    key32_of_score(i, lane / 32).  The two lanes of a query reduce their running max with
+//    one 32-lane swap.
+//  * O^T = V^T P^T per 16-key step: lane half h needs keys 8h .. 8h+7 of the step as its
+//    B operand, which is exactly what p32 put in its scores; the matching V^T fragment is
+//    one contiguous 16-byte read of a head-dim row.
+// ------------------------------------------------------------------------------------
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// key (within a 32-key block) held by A row r of a 32 x 32 score block
+AS_DEVICE int p32(int r) {
+  return ((r >> 4) & 1) * 16 + ((r >> 2) & 1) * 8 + ((r >> 3) & 1) * 4 + (r & 3);
+}
+// key (within the block) of score i = 4 j + e of a lane in half h: output row 8 j + 4 h + e
+AS_DEVICE int key32_of_score(int i, int h) {
+  const int j = i >> 2, e = i & 3;
+  return (j >> 1) * 16 + h * 8 + (j & 1) * 4 + e;
+}
+AS_DEVICE float halves_max(float v) {
+  auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+AS_DEVICE float halves_sum(float v) {
+  auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
+template <int HD, int NST>
+__global__ __launch_bounds__(512) void tree_attn_t32_kernel(
+    const f16 *__restrict__ qin, const bf16 *__restrict__ ck, const bf16 *__restrict__ cv,
+    TreeMeta meta, f16 *__restrict__ out, float *__restrict__ part_o,
+    float *__restrict__ part_ml, int n1, int H, int Hkv, int capacity, int nsplit, int rpg) {
+  constexpr int NW = 8;
+  constexpr int KS16 = HD / 16;   // 16-dim k-steps of a 32-row tile's S^T
+  constexpr int NDB = HD / 32;    // 32-dim blocks of its O^T
+  constexpr int KS32 = HD / 32;   // 32-dim k-steps of the remainder tile's S^T
+  constexpr int NB16 = HD / 16;   // 16-dim blocks of the remainder tile's O^T
+  constexpr int STAGE = 2 * KC * HD;
+  constexpr int L_DMA = HD / 4 / NW;
+  static_assert(NST >= 3, "the widening runs one stage ahead of the MFMAs");
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
+
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int G = H / Hkv, QR = G * n1;
+  const int nqg = (QR + rpg - 1) / rpg;
+  const int split = blockIdx.x / nqg, grp = blockIdx.x - split * nqg;
+  const int rlo = grp * rpg, rows = min(rpg, QR - rlo);
+  int n32 = rows >> 5, rem = rows & 31;
+  if (rem > 16) {  // a remainder beyond 16 rows is a (padded) 32-row tile of its own
+    ++n32;
+    rem = 0;
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lq = lane & 31, hh = lane >> 5;   // 32 x 32 layout: query column, lane half
+  const int lr = lane & 15, lg = lane >> 4;   // 16 x 16 layout (remainder tile)
+  const bool t32 = wave < n32;
+  const bool quarter = rem > 0 && wave >= NW - 4;
+  const int qk = wave & 3;                    // a quarter unit's key block in each chunk
+  const int S = meta.sess_S[b];
+  const int total = S + n1;
+  const int nchunks = (total + KC - 1) / KC;
+  const int cps = (nchunks + nsplit - 1) / nsplit;
+  const int c0 = split * cps;
+  const int c1 = min(nchunks, c0 + cps);
+  const bf16 *kb = ck + ((size_t)b * Hkv + g) * capacity * HD;
+  const bf16 *vb = cv + ((size_t)b * Hkv + g) * HD * capacity;
+  const size_t row0 = (size_t)b * n1;
+  const int q_stride = H * HD;
+  const float sscale = LOG2E / sqrtf((float)HD);
+  const float lazy = LAZY_LOG2 / sscale;
+
+  // This wave's 32-row tile: query rlo + 32 wave + lq.  Padding rows (and the tile of a
+  // wave without one) multiply zeros; their outputs are dropped.
+  f16x8 qf[KS16];
+  uint64_t anc;
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 o[NDB];
+  {
+    const int qv = rlo + wave * 32 + lq;
+    const bool pad = !t32 || qv >= rlo + rows;
+    const int qi = min(qv, QR - 1);
+    const int r = qi / G, h = g * G + (qi - r * G);
+    const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
+#pragma unroll
+    for (int s = 0; s < KS16; ++s) {
+      const f16x8 v = *(const f16x8 *)(qp + s * 16 + hh * 8);
+      qf[s] = pad ? f16x8{} : v;
+    }
+    anc = meta.anc[row0 + r];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+  }
+  // The remainder tile (quarter waves): query rlo + 32 n32 + lr.
+  f16x8 qq[KS32];
+  uint64_t ancq;
+  float mq = -INFINITY, lsq = 0.f;
+  f32x4 oq[NB16];
+  {
+    const int qv = rlo + n32 * 32 + lr;
+    const bool pad = !quarter || lr >= rem;
+    const int qi = min(qv, QR - 1);
+    const int r = qi / G, h = g * G + (qi - r * G);
+    const f16 *qp = qin + (row0 + r) * q_stride + h * HD;
+#pragma unroll
+    for (int s = 0; s < KS32; ++s) {
+      const f16x8 v = *(const f16x8 *)(qp + s * 32 + lg * 8);
+      qq[s] = pad ? f16x8{} : v;
+    }
+    ancq = meta.anc[row0 + r];
+#pragma unroll
+    for (int nb = 0; nb < NB16; ++nb) oq[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  wait_vmcnt<0>();   // the loop's vmcnt accounting covers the DMA only
+
+  auto stage_of = [&](int c) { return smem + ((c - c0) % NST) * STAGE; };
+  const int wt = tid, wstride = NW * 64;   // every wave widens its share
+
+  // Prologue: chunks c0 .. c0+NST-2 in flight, chunk c0 widened.
+#pragma unroll
+  for (int i = 0; i < NST - 1; ++i)
+    if (c0 + i < c1)
+      issue_chunk<HD, NW, true>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
+  if (c0 < c1) {
+    if (c0 + NST - 2 < c1) wait_vmcnt<(NST - 2) * L_DMA>(); else wait_vmcnt<0>();
+    lds_barrier();
+    widen_chunk<HD>(stage_of(c0), wt, wstride, c0 * KC, total);
+  }
+
+  // Fragment offsets (lane registers; blocks add compile-time constants): K row p32(lq)
+  // (+32 for the second key block) at piece 2 s + hh; V^T row lq (+32 db) at piece
+  // 2 ks + hh; the quarter unit's K row key_of_row(qk, lr) at piece 4 s + lg and its V^T
+  // half-piece.
+  const int krow = p32(lq), ksl = ksw32<HD>(krow);
+  int koff[KS16];
+#pragma unroll
+  for (int s = 0; s < KS16; ++s) koff[s] = krow * HD + (((s * 2 + hh) ^ ksl) << 3);
+  int voff[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) voff[ks] = lq * KC + (((ks * 2 + hh) ^ vsw(lq)) << 3);
+  const int qkey = key_of_row(qk, lr), qksl = ksw32<HD>(qkey);
+  int qkoff[KS32];
+#pragma unroll
+  for (int s = 0; s < KS32; ++s) qkoff[s] = qkey * HD + (((s * 4 + lg) ^ qksl) << 3);
+  const int qvoff = lr * KC + (((((qk >> 1) * 4) + lg) ^ vsw(lr)) << 3) + (qk & 1) * 4;
+
+  for (int c = c0; c < c1; ++c) {
+    if (c + 1 < c1) {
+      if (c + NST - 2 < c1) wait_vmcnt<(NST - 3) * L_DMA>(); else wait_vmcnt<0>();
+    }
+    chunk_barrier();
+    if (c + NST - 1 < c1)
+      issue_chunk<HD, NW, true>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity,
+                                wave, lane);
+    if (c + 1 < c1) widen_chunk<HD>(stage_of(c + 1), wt, wstride, (c + 1) * KC, total);
+
+    const uint16_t *st = stage_of(c);
+    const f16 *sk = (const f16 *)st;
+    const f16 *sv = (const f16 *)(st + KC * HD);
+    const int key0 = c * KC;
+    const bool tree_chunk = key0 + KC > S;
+    if (t32) {
+      // S^T for the chunk's two 32-key blocks: sc[kb][i] is the score of slot
+      // key0 + 32 kb + key32_of_score(i, hh) against this lane's query.  Both blocks are
+      // issued first; then each block gets its own online-softmax step and its P.V
+      // products, so block 0's softmax runs on the VALU while block 1's scores are still
+      // in the matrix pipe, and block 1's softmax while block 0's P.V runs.
+      f32x16 sc[2];
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sc[kb2][i] = 0.f;
+#pragma unroll
+        for (int s = 0; s < KS16; ++s) {
+          const f16x8 kf = *(const f16x8 *)(sk + koff[s] + kb2 * 32 * HD);
+          sc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qf[s], sc[kb2], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        SCHED_FENCE();
+        f32x16 &z = sc[kb2];
+        if (tree_chunk) {
+          MASK_BRANCH();
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int j = key0 + kb2 * 32 + key32_of_score(i, hh) - S;  // tree row, or < 0
+            const int sh = min(max(j - 1, 0), 63);
+            const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((anc >> sh) & 1ull)));
+            z[i] = vis ? z[i] : -INFINITY;
+          }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, z[i]);
+        mx = halves_max(mx);
+        const float m_new = lazy_ref(m_run, mx, lazy);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_use) * sscale);
+        m_run = m_new;
+        const float mb = m_use * sscale;
+        // the block's probabilities as the B operands of its two 16-key steps: step
+        // (j / 2) takes scores 4 j + e at positions (j % 2) * 4 + e
+        f16x8 pk[2];
+        float rs = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float pz = __builtin_amdgcn_exp2f(fmaf(z[i], sscale, -mb));
+          rs += pz;
+          const int j = i >> 2, e = i & 3;
+          pk[j >> 1][(j & 1) * 4 + e] = (f16)pz;
+        }
+        l_run = l_run * alpha + rs;
+        if (__ballot(alpha < 1.f)) {
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+        }
+#pragma unroll
+        for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+          for (int db = 0; db < NDB; ++db) {
+            const f16x8 va = *(const f16x8 *)(sv + voff[kb2 * 2 + k2] + db * 32 * KC);
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pk[k2], o[db], 0, 0, 0);
+          }
+      }
+      SCHED_FENCE();
+    }
+    if (quarter) {
+      // key block qk of the chunk for the remainder tile: 4 scores a lane
+      f32x4 sq = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS32; ++s) {
+        const f16x8 kf = *(const f16x8 *)(sk + qkoff[s]);
+        sq = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qq[s], sq, 0, 0, 0);
+      }
+      if (tree_chunk) {
+        MASK_BRANCH();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = key0 + key_of_score(qk, lg, e) - S;
+          const int sh = min(max(j - 1, 0), 63);
+          const bool vis = (j < 0) | ((j < n1) & ((j == 0) | (bool)((ancq >> sh) & 1ull)));
+          sq[e] = vis ? sq[e] : -INFINITY;
+        }
+      }
+      float mx = fmaxf(fmaxf(sq[0], sq[1]), fmaxf(sq[2], sq[3]));
+      mx = rows4_max(mx);
+      const float m_new = lazy_ref(mq, mx, lazy);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f((mq - m_use) * sscale);
+      mq = m_new;
+      const float mb = m_use * sscale;
+      f16x4 pq;
+      float rs = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sq[e], sscale, -mb));
+        rs += p;
+        pq[e] = (f16)p;
+      }
+      lsq = lsq * alpha + rs;
+      if (__ballot(alpha < 1.f)) {
+#pragma unroll
+        for (int nb = 0; nb < NB16; ++nb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) oq[nb][e] *= alpha;
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB16; ++nb) {
+        const f16x4 va = *(const f16x4 *)(sv + qvoff + nb * 16 * KC);
+        oq[nb] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, pq, oq[nb], 0, 0, 0);
+      }
+    }
+  }
+  wait_vmcnt<0>();
+
+  if (rem > 0) {
+    // Merge the remainder tile's four quarter units (the ring is free once every wave is
+    // past its last chunk); quarter wave qk finalises head-dim blocks qk * NB16/4 ...
+    __syncthreads();
+    f32x4 *mo = (f32x4 *)smem;                                 // [quarter][NB16][64 lanes]
+    float *mml = (float *)smem + (size_t)4 * NB16 * 64 * 4;    // [quarter][16 queries][2]
+    if (quarter) {
+      const float l = rows4_sum(lsq);
+#pragma unroll
+      for (int nb = 0; nb < NB16; ++nb) mo[(qk * NB16 + nb) * 64 + lane] = oq[nb];
+      if (lg == 0) {
+        mml[(qk * 16 + lr) * 2 + 0] = mq == -INFINITY ? -INFINITY : mq * sscale;
+        mml[(qk * 16 + lr) * 2 + 1] = l;
+      }
+    }
+    __syncthreads();
+    if (quarter) {
+      float mj[4], wj[4];
+      float M = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        mj[j] = mml[(j * 16 + lr) * 2];
+        M = fmaxf(M, mj[j]);
+      }
+      float L = 0.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        wj[j] = mj[j] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mj[j] - M);
+        L += wj[j] * mml[(j * 16 + lr) * 2 + 1];
+      }
+      const int qi = rlo + n32 * 32 + lr;
+      if (lr < rem) {
+        const int r = qi / G, h = g * G + (qi - r * G);
+        const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
+#pragma unroll
+        for (int i = 0; i < NB16 / 4; ++i) {
+          const int nb = qk * (NB16 / 4) + i;
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const f32x4 v = mo[(j * NB16 + nb) * 64 + lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[e] += wj[j] * v[e];
+          }
+          if (nsplit == 1) {
+            const float inv = L > 0.f ? 1.0f / L : 0.f;
+            f16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (f16)(acc[e] * inv);
+            *(f16x4 *)(out + (row0 + r) * (size_t)q_stride + h * HD + nb * 16 + lg * 4) = v;
+          } else {
+            *(f32x4 *)(part_o + (item * QR + qi) * HD + nb * 16 + lg * 4) = acc;
+          }
+        }
+        if (nsplit > 1 && qk == 0 && lg == 0) {
+          part_ml[(item * QR + qi) * 2 + 0] = M;
+          part_ml[(item * QR + qi) * 2 + 1] = L;
+        }
+      }
+    }
+  }
+
+  // o[db][4 j + e] is head dim 32 db + 8 j + 4 hh + e of query rlo + 32 wave + lq.
+  if (t32) {
+    const float l = halves_sum(l_run);
+    const int qi = rlo + wave * 32 + lq;
+    if (qi < rlo + rows) {
+      const int r = qi / G, h = g * G + (qi - r * G);
+      if (nsplit == 1) {
+        const float inv = l > 0.f ? 1.0f / l : 0.f;
+        f16 *op = out + (row0 + r) * (size_t)q_stride + h * HD + hh * 4;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            f16x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = (f16)(o[db][j * 4 + e] * inv);
+            *(f16x4 *)(op + db * 32 + j * 8) = v;
+          }
+      } else {
+        const size_t item = ((size_t)b * Hkv + g) * nsplit + split;
+        float *po = part_o + (item * QR + qi) * HD + hh * 4;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *(f32x4 *)(po + db * 32 + j * 8) =
+                f32x4{o[db][j * 4], o[db][j * 4 + 1], o[db][j * 4 + 2], o[db][j * 4 + 3]};
+        if (hh == 0) {
+          part_ml[(item * QR + qi) * 2 + 0] = m_run == -INFINITY ? -INFINITY : m_run * sscale;
+          part_ml[(item * QR + qi) * 2 + 1] = l;
+        }
+      }
+    }
+  }
+}
+
 // Merge of the split partials.  grid: (ceil(QR * HD / 4 / 256), kv heads, sessions); one
 // thread per 4 head dims of one query row.  part_ml holds (max in base-2 exponent units,
 // sum) per (item, query row).
@@ -549,19 +971,17 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
                                   int *nsplit_used) {
   const int G = H / Hkv, QR = G * n1;
   const int all_tiles = (QR + 15) / 16;
-  // A workgroup takes at most 32 query tiles (8 waves of up to 4); beyond that the tiles
-  // are dealt to ceil(tiles / 32) query groups of equal size (a 64-node tree under 8
-  // query heads per kv head: 520 rows, two groups of 17 tiles).
-  const int nqg = (all_tiles + 31) / 32;
-  const int tiles = (all_tiles + nqg - 1) / nqg;
-  // Up to 16 tiles: 16 waves, one tile per wave, the others widen (measured fastest on
-  // the 8B shape: 5 tiles); more tiles: 8 waves with up to 4 tiles each.
-  const int nw = tiles <= 16 ? 16 : 8;
-  const int upw = (tiles + nw - 1) / nw;
-  if (upw > 4 || capacity % KC != 0) return hipErrorInvalidValue;
-  // Key splits so that every resident workgroup slot of the chip gets work (one 16-wave
-  // workgroup per CU; two 8-wave ones at head_dim 64), keeping at least 4 chunks per split.
-  const int slots = cus * (nw == 8 && hd == 64 ? 2 : 1);
+  if (capacity % KC != 0) return hipErrorInvalidValue;
+  // Up to 16 tiles of 16 rows: 16 waves, one tile per wave, the others widen (measured
+  // fastest on the 8B shape: 5 tiles).  More rows: 8 waves of 32-row tiles plus a
+  // remainder of at most 16 rows, i.e. up to 272 rows a workgroup; beyond that the rows
+  // are dealt to query groups of equal size (8 query heads per kv head under a 64-node
+  // tree: 520 rows, two groups of 260), each streaming the key range once.
+  const bool t32 = all_tiles > 16;
+  const int nqg = t32 ? (QR + 271) / 272 : 1;
+  const int rpg = (QR + nqg - 1) / nqg;
+  // Key splits so that every CU gets a workgroup, keeping at least 4 chunks per split.
+  const int slots = cus;
   const int items = B * Hkv * nqg;
   const int nchunks = capacity / KC;
   int nsplit = (slots + items - 1) / items;
@@ -570,18 +990,22 @@ hipError_t launch_attention<bf16>(const f16 *q, const bf16 *ck, const bf16 *cv,
   while (nsplit > 1 && (long long)B * Hkv * nsplit * QR * hd > part_capacity) --nsplit;
   *nsplit_used = nsplit;
   const dim3 grid(nsplit * nqg, Hkv, B);
-#define GO(HD_, NW_, UPW_)                                                                \
-  launch_mfma<HD_, NW_, UPW_>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,  \
-                              capacity, nsplit, tiles)
-  // (more than 16 tiles means at least 3 a wave)
-  if (hd == 128) {
-    if (nw == 16) GO(128, 16, 1);
-    else if (upw == 3) GO(128, 8, 3); else GO(128, 8, 4);
+  if (t32) {
+    if (hd == 128)
+      hipLaunchKernelGGL((tree_attn_t32_kernel<128, AttnCfg<128>::NST>), grid, dim3(512), 0, s,
+                         q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv, capacity, nsplit,
+                         rpg);
+    else
+      hipLaunchKernelGGL((tree_attn_t32_kernel<64, AttnCfg<64>::NST>), grid, dim3(512), 0, s,
+                         q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv, capacity, nsplit,
+                         rpg);
+  } else if (hd == 128) {
+    launch_mfma<128, 16, 1>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,
+                            capacity, nsplit, all_tiles);
   } else {
-    if (nw == 16) GO(64, 16, 1);
-    else if (upw == 3) GO(64, 8, 3); else GO(64, 8, 4);
+    launch_mfma<64, 16, 1>(grid, s, q, ck, cv, meta, out, part_o, part_ml, n1, H, Hkv,
+                           capacity, nsplit, all_tiles);
   }
-#undef GO
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nsplit == 1) return e;
   const int cblocks = (QR * (hd / 4) + 255) / 256;

@@ -63,6 +63,8 @@ _STEP = [
     ("fixup_resid_norm_kernel", "+"),
     ("at::native::elementwise_kernel", None),
     ("gemm_f16w_kernelILi4EDF16b", "gemm_qkv"),
+    ("tree_attn_t32_kernelILi128E", "tree_attention"),
+    ("attn_combine_kernel", "+"),
     ("gemm_f16w_kernelILi5EDF16b", "gemm_lm_head"),
     ("vocab_verify_kernel", "vocab_verify"),
 ]
