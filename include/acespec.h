@@ -83,11 +83,20 @@ typedef struct {
   const void *w_down;      /* [d_model, d_ff]                                         */
 } acespec_layer_weights;
 
+/* Storage of the dense matrices of a bf16 model (wqkv, wo, w_gate_up, w_down, lm_head).
+ * The embedding and the RMSNorm gains are always row-major in the model dtype. */
+typedef enum {
+  ACESPEC_LAYOUT_ROWS = 0,    /* bf16, row-major [out, in] as above                       */
+  ACESPEC_LAYOUT_PACKED = 1   /* fp16 in the fragment order of acespec_pack_weight (same
+                                 size); bf16 models only, vocab a multiple of 16           */
+} acespec_layout;
+
 typedef struct {
   const void *embed;                     /* [vocab, d_model]                           */
   const acespec_layer_weights *layers;   /* HOST array of n_layers entries              */
   const void *final_norm;                /* [d_model]                                  */
   const void *lm_head;                   /* [vocab, d_model]                           */
+  acespec_layout layout;                 /* of the dense matrices; 0 = row-major        */
 } acespec_weights;
 
 /* KV cache, in the model dtype.  Keys: k [n_layers][B][n_kv_heads][capacity][head_dim],
@@ -236,6 +245,20 @@ int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_h
 int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_t *path,
                       const int32_t *path_len, const int32_t *status, int B, int N,
                       int32_t *new_prefix_len, hipStream_t stream);
+
+/* Re-lays one row-major bf16 weight matrix [rows, cols] (rows % 16 == 0, cols % 32 == 0)
+ * out into the packed layout (ACESPEC_LAYOUT_PACKED): for every 16-row block and 32-column
+ * step, the 1 KB operand of one 16x16x32 matrix-core instruction, contiguous, its values
+ * widened to fp16.  The packed matrix holds the operands the verify pass multiplies by
+ * anyway (the row-major path widens each bf16 weight to fp16 the same way before its
+ * products, so the two layouts differ at most in how a product's k-slices are summed in
+ * fp32); packed, each wave of the GEMMs loads its weight operands straight into
+ * registers, and only the activations pass through LDS.  Weights
+ * beyond the fp16 range (|w| > 65504) become +-inf, as they do on the row-major path.
+ * Not part of the verify step: a caller packs its weights once (e.g. at load time).
+ *  src [rows, cols] bf16, dst rows*cols*2 bytes; both DEVICE, caller-owned, no overlap.
+ * Enqueued on stream; ACESPEC_EINVAL for a NULL pointer or a shape outside the above. */
+int acespec_pack_weight(const void *src, void *dst, int rows, int cols, hipStream_t stream);
 
 /* Message for the last non-OK return on this thread ("" if none). */
 const char *acespec_last_error(void);

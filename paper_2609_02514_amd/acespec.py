@@ -21,7 +21,7 @@ ACESPEC_F32, ACESPEC_BF16 = 0, 1
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",
             "acespec_verify_tree_scalar_q", "acespec_verify_tail", "acespec_commit_kv",
             "acespec_last_error", "acespec_timing_enable", "acespec_timing_read",
-            "acespec_timing_only", "acespec_verify_tail_noalloc"]
+            "acespec_timing_only", "acespec_verify_tail_noalloc", "acespec_pack_weight"]
 
 
 class ModelDesc(C.Structure):
@@ -36,9 +36,12 @@ class LayerWeights(C.Structure):
                 ("mlp_norm", C.c_void_p), ("w_gate_up", C.c_void_p), ("w_down", C.c_void_p)]
 
 
+ACESPEC_LAYOUT_ROWS, ACESPEC_LAYOUT_PACKED = 0, 1
+
+
 class Weights(C.Structure):
     _fields_ = [("embed", C.c_void_p), ("layers", C.POINTER(LayerWeights)),
-                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p), ("layout", C.c_int)]
 
 
 class KVCache(C.Structure):
@@ -95,6 +98,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.acespec_commit_kv.argtypes = [C.c_void_p, C.POINTER(KVCache), C.c_void_p, C.c_void_p,
                                       C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
     lib.acespec_commit_kv.restype = C.c_int
+    lib.acespec_pack_weight.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_void_p]
+    lib.acespec_pack_weight.restype = C.c_int
     lib.acespec_last_error.argtypes = []
     lib.acespec_last_error.restype = C.c_char_p
     lib.acespec_timing_enable.argtypes = [C.c_void_p, C.c_int]
@@ -180,6 +185,10 @@ def acespec_commit_kv(ctx, kv: KVCache, path: int, path_len: int, status: Option
                                            new_prefix_len, stream))
 
 
+def acespec_pack_weight(src: int, dst: int, rows: int, cols: int, stream: int) -> int:
+    return _check(load().acespec_pack_weight(src, dst, rows, cols, stream))
+
+
 def acespec_timing_enable(ctx, enable: bool) -> None:
     _check(load().acespec_timing_enable(ctx, 1 if enable else 0))
 
@@ -236,6 +245,26 @@ class Verifier:
         except Exception:
             pass
 
+    DENSE = ("wqkv", "wo", "w_gate_up", "w_down")
+
+    def pack_weights(self, W):
+        """A copy of W whose dense matrices (the DENSE ones of every layer and the LM head)
+        are in the packed layout (acespec_pack_weight); the embedding and the norm gains
+        are shared with W.  The result carries `packed = True` for weights_struct."""
+        import copy
+        import torch
+
+        def pk(t):
+            out = torch.empty(t.numel(), dtype=torch.float16, device=t.device)
+            acespec_pack_weight(_ptr(t), _ptr(out), t.shape[0], t.shape[1], self._stream())
+            return out
+
+        P = copy.copy(W)
+        P.layers = [dict(lw, **{k: pk(lw[k]) for k in self.DENSE}) for lw in W.layers]
+        P.lm_head = pk(W.lm_head)
+        P.packed = True
+        return P
+
     def weights_struct(self, W) -> Weights:
         layers = (LayerWeights * max(1, len(W.layers)))()
         for i, lw in enumerate(W.layers):
@@ -243,7 +272,8 @@ class Verifier:
                                      _ptr(lw["mlp_norm"]), _ptr(lw["w_gate_up"]),
                                      _ptr(lw["w_down"]))
         self._keep.append(layers)
-        return Weights(_ptr(W.embed), layers, _ptr(W.final_norm), _ptr(W.lm_head))
+        layout = ACESPEC_LAYOUT_PACKED if getattr(W, "packed", False) else ACESPEC_LAYOUT_ROWS
+        return Weights(_ptr(W.embed), layers, _ptr(W.final_norm), _ptr(W.lm_head), layout)
 
     @staticmethod
     def alloc_outputs(rows: int, sessions: int, n1: int, k: int, V: int, device,

@@ -156,7 +156,8 @@ int verify_tree_impl(acespec_ctx *ctx, const acespec_weights *w, const acespec_k
   const int F = d.d_ff, V = d.vocab, QKVN = (H + 2 * Hkv) * hd;
   const int cap = kv->capacity;
   A *x_a = (A *)ctx->a, *x_attn = (A *)ctx->attn, *x_q = (A *)ctx->q, *x_h = (A *)ctx->h;
-  const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus};
+  const GemmAux aux{ctx->gpart, ctx->gpart_cap, ctx->cus,
+                   w->layout == ACESPEC_LAYOUT_PACKED ? 1 : 0};
   float *logits = o->logits_out ? o->logits_out : ctx->logits;
   const TreeMeta &meta = ctx->meta;
 
@@ -453,6 +454,11 @@ int verify_tree_checked(acespec_ctx *ctx, const acespec_weights *w, const acespe
     if (!lw.attn_norm || !lw.wqkv || !lw.wo || !lw.mlp_norm || !lw.w_gate_up || !lw.w_down)
       return fail(ACESPEC_EINVAL, "layer %d has a NULL weight pointer", l);
   }
+  if (w->layout != ACESPEC_LAYOUT_ROWS && w->layout != ACESPEC_LAYOUT_PACKED)
+    return fail(ACESPEC_EINVAL, "unknown weight layout %d", (int)w->layout);
+  if (w->layout == ACESPEC_LAYOUT_PACKED && (d.dtype != ACESPEC_BF16 || d.vocab % 16 != 0))
+    return fail(ACESPEC_EUNSUPPORTED,
+                "packed weights need a bf16 model with a vocabulary that is a multiple of 16");
   if (!kv->k || !kv->v || !kv->prefix_len) return fail(ACESPEC_EINVAL, "kv cache pointer NULL");
   if (B < 1 || B > ctx->max_batch)
     return fail(ACESPEC_EINVAL, "B must be in [1, %d] (got %d)", ctx->max_batch, B);
@@ -502,6 +508,20 @@ int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *w,
   }
   return verify_tree_checked(ctx, w, kv, tree_tokens, parent_idx, nullptr, q_hat, uniforms, B,
                              N, p, o, stream);
+}
+
+int acespec_pack_weight(const void *src, void *dst, int rows, int cols, hipStream_t stream) {
+  g_err.clear();
+  if (!src || !dst) return fail(ACESPEC_EINVAL, "src or dst is NULL");
+  if (rows < 16 || cols < 32 || rows % 16 != 0 || cols % 32 != 0)
+    return fail(ACESPEC_EINVAL, "rows must be a positive multiple of 16 and cols of 32 (got %d x %d)",
+                rows, cols);
+  const char *s0 = (const char *)src, *d0 = (const char *)dst;
+  const size_t bytes = (size_t)rows * cols * 2;
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(ACESPEC_EINVAL, "src and dst overlap");
+  const hipError_t e = launch_pack_weights((const bf16 *)src, (f16 *)dst, rows, cols, stream);
+  if (e != hipSuccess) return fail(ACESPEC_EHIP, "pack launch: %s", hipGetErrorString(e));
+  return ACESPEC_OK;
 }
 
 int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,

@@ -188,6 +188,7 @@ struct GemmAux {
   float *part;
   long long part_cap;
   int cus;
+  int packed = 0;  // W is in the packed fragment order of launch_pack_weights
 };
 // Where the QKV projection's RoPE epilogue puts its results: rotated queries (activation
 // type, [rows, H*hd]) and the tree rows' keys and values in their cache slots.
@@ -235,7 +236,12 @@ hipError_t launch_gemm_resid_norm(const TA *A, const TW *W, int M, int N, int K,
 template <typename TB>
 hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
                                const TB *W, int M, int N, int K, f16 *out, float *outf,
-                               float *part, long long part_cap, int cus, hipStream_t s);
+                               float *part, long long part_cap, int cus, hipStream_t s,
+                               int packed = 0);
+
+// Packs a row-major bf16 weight matrix [rows, K] (rows % 16 == 0, K % 32 == 0) into the
+// fp16 MFMA-fragment order the packed GEMM path reads (same byte size).
+hipError_t launch_pack_weights(const bf16 *W, f16 *P, int rows, int K, hipStream_t s);
 
 // Exact widening of a bf16 tensor to fp16 (in range), n elements.
 hipError_t launch_cast_bf16_f16(const bf16 *in, f16 *out, size_t n, hipStream_t s);

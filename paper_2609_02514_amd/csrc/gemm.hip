@@ -67,7 +67,24 @@ template <int ROWB> AS_DEVICE int piece_off(int row, int pc) {
   return row * ROWB + ((pc ^ sw) << 4);
 }
 
-template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int OCC, int KSS>
+// Epilogue LDS needs beyond the operand ring: the QKV RoPE epilogue stages 64-row parts
+// of the fp32 tile (plus a row table), the row-maximum epilogue one float per (wave
+// column, tile row).
+constexpr int epi_smem(int epi, int tbm, int tbn, int wnn) {
+  return epi == acespec::EPI_QKV_ROPE ? 64 * (tbn + 4) * 4 + 64 * 8
+         : epi == acespec::EPI_F32_MAX ? wnn * tbm * 4
+                                        : 0;
+}
+
+// PK = 0: W is row-major [N, K] and staged through LDS with the activations.
+// PK = 1: W is pre-packed fp16 in MFMA fragment order (pack_frag_kernel): each wave loads
+//   its own weight fragments straight into registers, NST - 1 k-steps ahead, and only the
+//   activations go through LDS.  A packed fragment is 1 KB of contiguous memory, so these
+//   loads are as cheap for the address unit as the row-contiguous DMA, while LDS carries a
+//   third of the bytes (no weight rows written, no weight fragments read) and no widening
+//   instructions run.  KSS = 32 only.
+template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int OCC, int KSS,
+          int PK>
 __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
@@ -75,16 +92,22 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   constexpr int NW = WMN * WNN;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
   constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
-  constexpr int A_BYTES = TBM * ROWB, B_BYTES = TBN * ROWB;
+  constexpr int A_BYTES = TBM * ROWB, B_BYTES = PK ? 0 : TBN * ROWB;
   constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
-  constexpr int A_DMA = A_BYTES / 1024 / NW, B_DMA = B_BYTES / 1024 / NW;
+  // 1 KB DMA blocks of the A tile per wave (rounded up: a wave past the last block loads
+  // the last block again, the same bytes to the same place, so every wave issues the same
+  // number of loads and the vmcnt arithmetic below holds for all of them)
+  constexpr int A_BLKS = A_BYTES / 1024, A_DMA = (A_BLKS + NW - 1) / NW;
+  constexpr int B_DMA = B_BYTES / 1024 / NW;
   constexpr int L_DMA = A_DMA + B_DMA;
   constexpr int KSUB = KSS / 32;            // 32-wide MFMA k steps per stage
   constexpr int F = KSUB * WTM;             // A fragments per stage, in use order
-  static_assert(A_DMA * 1024 * NW == A_BYTES && B_DMA * 1024 * NW == B_BYTES, "DMA split");
+  static_assert(A_BLKS * 1024 == A_BYTES && B_DMA * 1024 * NW == B_BYTES, "DMA split");
   static_assert(F >= 4 && NST >= 3, "pipeline shape");
+  static_assert(!PK || KSS == 32, "packed weights come in 32-wide k steps");
   constexpr int HALF = WTN / 2;  // SwiGLU: gate blocks, then the matching up blocks
-  __shared__ __attribute__((aligned(1024))) char smem[NST * STAGE_BYTES];
+  constexpr int RING = NST * STAGE_BYTES, EPI_SM = epi_smem(EPI, TBM, TBN, WNN);
+  __shared__ __attribute__((aligned(1024))) char smem[RING > EPI_SM ? RING : EPI_SM];
   typedef typename Vec8<TB>::type tbx8;
 
   // Units: `full` whole tiles, then tsplit k-slices of each remaining tile (their partial
@@ -125,10 +148,11 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   const int wrows = EPI == acespec::EPI_SWIGLU ? 2 * N : N;
   const __amdgpu_buffer_rsrc_t rsb = make_rsrc(W, (uint32_t)((size_t)wrows * K * 2));
   const int drow = lane / PIECES, dpc = lane % PIECES;
-  uint32_t va[A_DMA], vb[B_DMA];
+  uint32_t va[A_DMA], vb[B_DMA > 0 ? B_DMA : 1];
 #pragma unroll
   for (int t = 0; t < A_DMA; ++t) {
-    const int lrow = (w * A_DMA + t) * ROWS_PER_BLK + drow;
+    const int blk = w * A_DMA + t < A_BLKS ? w * A_DMA + t : A_BLKS - 1;
+    const int lrow = blk * ROWS_PER_BLK + drow;
     const int r = m0 + lrow;
     va[t] = r < M ? (uint32_t)r * K * 2 + (piece_off<ROWB>(lrow, dpc) - lrow * ROWB)
                   : (uint32_t)M * K * 2;
@@ -147,12 +171,32 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     }
     vb[t] = (uint32_t)wr * K * 2 + (piece_off<ROWB>(row, dpc) - row * ROWB);
   }
+  // Packed weights: fragment (16-row block nb, k step kt) at ((nb * KT + kt) * 64 + lane)
+  // 16-byte units; the wave's WTN column blocks, SwiGLU-paired like the LDS path's rows.
+  const f16x8 *pkw[PK ? WTN : 1];
+  if constexpr (PK) {
+#pragma unroll
+    for (int j = 0; j < WTN; ++j) {
+      int c, base;
+      if (EPI == acespec::EPI_SWIGLU) {
+        c = tn * (TBN / 2) + wn * HALF * 16 + (j < HALF ? j : j - HALF) * 16;
+        c = c < N ? c : N - 16;
+        base = j < HALF ? c : N + c;
+      } else {
+        c = tn * TBN + wn * WTN * 16 + j * 16;
+        base = c < N ? c : N - 16;
+      }
+      pkw[j] = (const f16x8 *)W + (size_t)(base >> 4) * KT * 64 + lane;
+    }
+  }
   auto issue = [&](int kt, int stage) {
     char *base = smem + stage * STAGE_BYTES;
     const int soff = kt * ROWB;
 #pragma unroll
-    for (int t = 0; t < A_DMA; ++t)
-      buf_dma16(rsa, (lds_ptr_t)(base + (w * A_DMA + t) * 1024), va[t], soff);
+    for (int t = 0; t < A_DMA; ++t) {
+      const int blk = w * A_DMA + t < A_BLKS ? w * A_DMA + t : A_BLKS - 1;
+      buf_dma16(rsa, (lds_ptr_t)(base + blk * 1024), va[t], soff);
+    }
 #pragma unroll
     for (int t = 0; t < B_DMA; ++t)
       buf_dma16(rsb, (lds_ptr_t)(base + A_BYTES + (w * B_DMA + t) * 1024), vb[t], soff);
@@ -180,6 +224,47 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
 #pragma unroll
     for (int j = 0; j < WTN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  if constexpr (PK) {
+    // Step i: A k-tile i sits in ring slot i % NST, its weight fragments in register set
+    // i % NST (the loop is unrolled NST times so the set index is static).  At the top of
+    // a step this wave's loads of step i have landed (NST - 2 newer steps may be out);
+    // after the barrier every wave's have, and every wave is done with slot i - 1, which
+    // the loads of step i + NST - 1 then refill.
+    constexpr int L_VM = A_DMA + WTN;
+    f16x8 rb[NST][WTN], fa[F];
+#pragma unroll
+    for (int p = 0; p < NST - 1; ++p) {
+      const int kt = kt0 + (p < nk ? p : nk - 1);
+      issue(kt, p);
+#pragma unroll
+      for (int j = 0; j < WTN; ++j) rb[p][j] = pkw[j][(size_t)kt * 64];
+    }
+    for (int i0 = 0; i0 < nk; i0 += NST) {
+#pragma unroll
+      for (int u = 0; u < NST; ++u) {
+        if (i0 + u >= nk) break;
+        wait_vmcnt<(NST - 2) * L_VM>();
+        __builtin_amdgcn_s_barrier();
+        const int kn = kt0 + (i0 + u + NST - 1 < nk ? i0 + u + NST - 1 : nk - 1);
+        issue(kn, (u + NST - 1) % NST);
+#pragma unroll
+        for (int j = 0; j < WTN; ++j) rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)kn * 64];
+        const char *sc = smem + u * STAGE_BYTES;
+        fa[0] = *(const f16x8 *)(sc + aoff[0]);
+        fa[1] = *(const f16x8 *)(sc + aoff[1]);
+        fa[2] = *(const f16x8 *)(sc + aoff[2]);
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+          if (f + 3 < F) fa[f + 3] = *(const f16x8 *)(sc + aoff[f + 3]);
+          SCHED_FENCE();
+#pragma unroll
+          for (int j = 0; j < WTN; ++j)
+            acc[f][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[f], rb[u][j], acc[f][j], 0, 0, 0);
+          SCHED_FENCE();
+        }
+      }
+    }
+  } else {
   for (int p = 0; p < NST - 1; ++p) issue(kt0 + (p < nk ? p : nk - 1), p);
   wait_vmcnt<(NST - 2) * L_DMA>();  // stage 0 landed for this wave
   __builtin_amdgcn_s_barrier();
@@ -227,6 +312,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
       }
     }
   }
+  }
   // No LDS DMA may still be writing when the workgroup's LDS is released.
   wait_vmcnt<0>();
 
@@ -235,8 +321,8 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     // 64-row parts so that each head's rotation pairs (i, i + hd/2) and each value
     // column's run of consecutive tree slots can be read across waves.
     constexpr int CR = 64, SP = TBN + 4;  // rows per part, row pitch in floats
-    static_assert(CR * SP * 4 + CR * 8 <= NST * STAGE_BYTES,
-                  "a part of the tile and its row table fit the ring");
+    static_assert(CR * SP * 4 + CR * 8 <= sizeof(smem),
+                  "a part of the tile and its row table fit the workgroup's LDS");
     float *st = (float *)smem;
     int *rsess = (int *)(st + CR * SP);  // per row of the part: its session,
     int *rslot = rsess + CR;             // and the cache slot of its tree row
@@ -569,6 +655,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float *__restrict__
   }
 }
 
+// Packs a row-major bf16 weight matrix [rows, K] into the fp16 fragment order the packed
+// GEMM path loads: 16-byte unit u = (nb * (K / 32) + kt) * 64 + l holds row nb * 16 + l % 16,
+// columns kt * 32 + (l / 16) * 8 .. + 8 (the B operand of one v_mfma_f32_16x16x32_f16 per
+// 64 units).  The widening is exact in the fp16 normal range (the same conversion the
+// row-major path applies in registers), so both layouts give identical products.
+__global__ __launch_bounds__(256) void pack_frag_kernel(const bf16 *__restrict__ W,
+                                                        f16 *__restrict__ P, int rows, int K) {
+  const long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int KT = K >> 5;
+  if (u >= (long long)(rows >> 4) * KT * 64) return;
+  const int l = (int)(u & 63);
+  const long long fr = u >> 6;
+  const int kt = (int)(fr % KT), nb = (int)(fr / KT);
+  const bf16x8 v = *(const bf16x8 *)(W + (size_t)(nb * 16 + (l & 15)) * K + kt * 32 + (l >> 4) * 8);
+  *(f16x8 *)(P + u * 8) = bf16x8_to_f16x8(v);
+}
+
 using acespec::EPI_STORE;
 using acespec::EPI_RESID;
 using acespec::EPI_SWIGLU;
@@ -585,14 +688,20 @@ using acespec::EPI_F32_MAX;
 // and 256 x 256 tiles on 32 x 32 MFMAs with one wave per SIMD (128 x 128 wave tiles: the
 // single wave cannot cover the barrier and DMA waits).
 struct GemmVariant {
-  int wmn, wnn, wtm, wtn, nst, occ, kss;
+  int wmn, wnn, wtm, wtn, nst, occ, kss, pk;
 };
 constexpr GemmVariant kVariants[] = {
-    {1, 4, 8, 4, 3, 2, 32},   // 0: 128 x 256, 4 waves of 128 x 64, 72 KB LDS, 2 WGs per CU
-    {2, 2, 4, 4, 4, 2, 32},   // 1: 128 x 128, 4 waves of 64 x 64, 64 KB LDS, 2 WGs per CU
-    {2, 4, 4, 4, 3, 1, 64},   // 2: 128 x 256, 8 waves of 64 x 64, k 64, 144 KB LDS, 1 WG per CU
-    {2, 4, 8, 4, 4, 1, 32},   // 3: 256 x 256, 8 waves of 128 x 64, 128 KB LDS, 1 WG per CU
-    {2, 2, 9, 2, 3, 1, 64},   // 4: 288 x 64, 4 waves of 144 x 32, k 64, 132 KB LDS, 1 WG per CU
+    {1, 4, 8, 4, 3, 2, 32, 0},  // 0: 128 x 256, 4 waves of 128 x 64, 72 KB LDS, 2 WGs per CU
+    {2, 2, 4, 4, 4, 2, 32, 0},  // 1: 128 x 128, 4 waves of 64 x 64, 64 KB LDS, 2 WGs per CU
+    {2, 4, 4, 4, 3, 1, 64, 0},  // 2: 128 x 256, 8 waves of 64 x 64, k 64, 144 KB LDS, 1 WG per CU
+    {2, 4, 8, 4, 4, 1, 32, 0},  // 3: 256 x 256, 8 waves of 128 x 64, 128 KB LDS, 1 WG per CU
+    {2, 2, 9, 2, 3, 1, 64, 0},  // 4: 288 x 64, 4 waves of 144 x 32, k 64, 132 KB LDS, 1 WG per CU
+    // packed weights (registers fed straight from the fragment-ordered copy):
+    {1, 4, 8, 4, 4, 2, 32, 1},  // 5: 128 x 256, 4 waves of 128 x 64, 32 KB ring, 2 WGs per CU
+    {2, 4, 8, 4, 4, 1, 32, 1},  // 6: 256 x 256, 8 waves of 128 x 64, 64 KB ring, 1 WG per CU
+    {2, 2, 4, 4, 4, 2, 32, 1},  // 7: 128 x 128, 4 waves of 64 x 64, 32 KB ring, 2 WGs per CU
+    {2, 2, 9, 2, 4, 1, 32, 1},  // 8: 288 x 64, 4 waves of 144 x 32, 72 KB ring, 1 WG per CU
+    {2, 4, 4, 4, 4, 1, 32, 1},  // 9: 128 x 256, 8 waves of 64 x 64, 32 KB ring, 1 WG per CU
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -642,7 +751,7 @@ void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int 
   const int tiles = mt * nt;
   const int units = sp.full + (tiles - sp.full) * sp.tsplit;
   hipLaunchKernelGGL(
-        (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss>),
+        (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss, v.pk>),
         dim3(units), dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
         sp.full, sp.tsplit, ro, tmax);
   if (sp.tsplit > 1) {
@@ -662,7 +771,7 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
                 float *tmax = nullptr) {
   switch (var) {
 #define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax); break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
 #undef CASE
     default: break;
   }
@@ -674,8 +783,18 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
 // for the residual and LM-head products once there are enough rows, 128 x 256 otherwise
 // (for the gate/up product at ~1k rows both tilings measure the same, the 256 x 256 one
 // only with its last round sliced).
-int pick_variant(int epi, int M, int N, int K) {
+int pick_variant(int epi, int M, int N, int K, int packed) {
   (void)K;
+  if (packed) {
+    // measured on MI355X in the verify steps (272 - 4096 rows): 128 x 256 tiles for most
+    // products; 288 x 64 (gate/up) and 128 x 128 tiles for few-row batches, 256 x 256
+    // (fewer operand bytes per flop) for the residual products of ~1k rows and for
+    // thousands of rows
+    if (M <= 288 && epi == EPI_SWIGLU) return 8;
+    if (M <= 384) return 7;
+    if (M >= 2048 || (M >= 1024 && epi == EPI_RESID)) return 6;
+    return 5;
+  }
   // gate/up with up to 288 rows (a 16-session 1B-class batch: 272): one tile spans every
   // row, so each weight panel is read once and the product is one tile per CU (10 % faster
   // there; for the residual products, which are sliced along K, it measured slower)
@@ -693,9 +812,10 @@ namespace acespec {
 template <typename TB>
 hipError_t launch_f16w_variant(int var, int splits_override, int epi, const f16 *A,
                                const TB *W, int M, int N, int K, f16 *out, float *outf,
-                               float *part, long long part_cap, int cus, hipStream_t s) {
-  if (var < 0) var = pick_variant(epi, M, N, K);
-  if (var >= kNumVariants) return hipErrorInvalidValue;
+                               float *part, long long part_cap, int cus, hipStream_t s,
+                               int packed) {
+  if (var < 0) var = pick_variant(epi, M, N, K, packed);
+  if (var >= kNumVariants || kVariants[var].pk != (packed ? 1 : 0)) return hipErrorInvalidValue;
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm;
@@ -728,7 +848,7 @@ template <>
 hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
                                              float *x, const bf16 *gain, f16 *out, float eps,
                                              const GemmAux &aux, hipStream_t s) {
-  const int var = pick_variant(EPI_RESID, M, N, K);
+  const int var = pick_variant(EPI_RESID, M, N, K, aux.packed);
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
@@ -736,7 +856,7 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
       plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
   if (sp.full != 0 || sp.tsplit < 2 || N % tbn != 0 || N > 8 * 4 * 256) {
     hipError_t e = launch_f16w_variant<bf16>(var, 0, EPI_RESID, A, W, M, N, K, nullptr, x,
-                                             aux.part, aux.part_cap, aux.cus, s);
+                                             aux.part, aux.part_cap, aux.cus, s, aux.packed);
     if (e != hipSuccess) return e;
     return launch_rmsnorm<bf16, float>(x, gain, out, M, N, eps, s);
   }
@@ -746,13 +866,14 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
   case VV: {                                                                                \
     constexpr GemmVariant g = kVariants[VV];                                                \
     hipLaunchKernelGGL(                                                                     \
-        (gemm_f16w_kernel<EPI_RESID, bf16, g.wmn, g.wnn, g.wtm, g.wtn, g.nst, g.occ, g.kss>), \
+        (gemm_f16w_kernel<EPI_RESID, bf16, g.wmn, g.wnn, g.wtm, g.wtn, g.nst, g.occ, g.kss,  \
+                          g.pk>),                                                           \
         dim3(mt * nt * sp.tsplit), dim3(g.wmn * g.wnn * 64), 0, s, A, W, M, N, K, nullptr,   \
         x, aux.part, mt, nt, 0, sp.tsplit, RopeOut<bf16>{}, nullptr);                       \
     launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
     break;                                                                                  \
   }
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
 #undef CASE
     default: return hipErrorInvalidValue;
   }
@@ -761,13 +882,21 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
 
 template hipError_t launch_f16w_variant<bf16>(int, int, int, const f16 *, const bf16 *, int, int,
                                               int, f16 *, float *, float *, long long, int,
-                                              hipStream_t);
+                                              hipStream_t, int);
+
+hipError_t launch_pack_weights(const bf16 *W, f16 *P, int rows, int K, hipStream_t s) {
+  if (rows <= 0 || K <= 0 || rows % 16 != 0 || K % 32 != 0) return hipErrorInvalidValue;
+  const long long units = (long long)(rows / 16) * (K / 32) * 64;
+  hipLaunchKernelGGL(pack_frag_kernel, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, s, W,
+                     P, rows, K);
+  return hipGetLastError();
+}
 
 template <>
 hipError_t launch_gemm<bf16, f16>(int epi, const f16 *A, const bf16 *W, int M, int N, int K,
                                   f16 *out, float *outf, const GemmAux &aux, hipStream_t s) {
   return launch_f16w_variant<bf16>(-1, 0, epi, A, W, M, N, K, out, outf, aux.part,
-                                   aux.part_cap, aux.cus, s);
+                                   aux.part_cap, aux.cus, s, aux.packed);
 }
 
 template <>
@@ -808,19 +937,21 @@ template <>
 hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
                                       float *qkv, const RopeOut<bf16> &ro, const TreeMeta &meta,
                                       int B, const GemmAux &aux, hipStream_t s) {
-  const int var = pick_variant(EPI_F32, M, N, K);
+  // packed weights: 128 x 256 tiles of eight 64 x 64 waves, kept whole when they fill most
+  // CUs, so the RoPE and cache write stay in the epilogue
+  const int var = aux.packed ? (M <= 384 ? 7 : 9) : pick_variant(EPI_F32, M, N, K, 0);
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
-  const SplitPlan sp =
-      plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  SplitPlan sp = plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  if (aux.packed && 4 * mt * nt >= 3 * aux.cus * v.occ) sp = SplitPlan{mt * nt, 1};
   if (sp.tsplit == 1 && tbn % ro.hd == 0 && N == (ro.H + 2 * ro.Hkv) * ro.hd) {
     launch_epi<EPI_QKV_ROPE, bf16>(var, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
                                    sp, ro);
     return hipGetLastError();
   }
   hipError_t e = launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, qkv,
-                                           aux.part, aux.part_cap, aux.cus, s);
+                                           aux.part, aux.part_cap, aux.cus, s, aux.packed);
   if (e != hipSuccess) return e;
   return launch_rope_kv<bf16>(qkv, ro.q, meta, ro.ck, ro.cv, B, ro.n1, ro.H, ro.Hkv, ro.hd,
                               ro.capacity, ro.rot, s);
@@ -842,7 +973,7 @@ hipError_t launch_lm_head<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, 
                                      float *logits, float *tile_max, int *ntile,
                                      const GemmAux &aux, hipStream_t s) {
   *ntile = 0;
-  const int var = pick_variant(EPI_F32, M, N, K);
+  const int var = pick_variant(EPI_F32, M, N, K, aux.packed);
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
@@ -850,7 +981,7 @@ hipError_t launch_lm_head<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, 
       plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
   if (tile_max == nullptr || (sp.tsplit > 1 && (tbn / 4) > 64))
     return launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, logits, aux.part,
-                                     aux.part_cap, aux.cus, s);
+                                     aux.part_cap, aux.cus, s, aux.packed);
   launch_epi<EPI_F32_MAX, bf16>(var, s, A, W, M, N, K, nullptr, logits, aux.part, mt, nt, sp,
                                 RopeOut<bf16>{}, tile_max);
   *ntile = nt;

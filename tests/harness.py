@@ -80,7 +80,7 @@ class TreeRun:
 
 
 def run_tree(w: synth.Workload, seed=None, sessions: Sequence[int] = None, device="cuda",
-             weights=None, keep_logits=True, verifier=None) -> TreeRun:
+             weights=None, keep_logits=True, verifier=None, packed=False) -> TreeRun:
     from paper_2609_02514_amd.acespec import Verifier
     seed = w.seed_base if seed is None else seed
     log(f"gen {w.name} seed={seed} L={w.L} d={w.d} V={w.V} B={w.B} S={w.S} tree={w.tree}")
@@ -91,12 +91,16 @@ def run_tree(w: synth.Workload, seed=None, sessions: Sequence[int] = None, devic
     hin = dict(tokens=host(batch.tokens), parents=host(batch.parents),
                prefix_len=host(batch.prefix_len), q=host(batch.q), u=host(batch.u))
     v = verifier or Verifier.for_workload(w)
-    ws = v.weights_struct(W)
+    # packed: the GPU multiplies by the packed copy of W's dense matrices; the oracle
+    # keeps reading W itself
+    Wg = v.pack_weights(W) if packed else W
+    ws = v.weights_struct(Wg)
     outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, device, keep_logits)
     log(f"verify_tree B={B} N={n1 - 1} cap={batch.cap}")
     v.verify_tree(ws, batch.kv_k, batch.kv_v, batch.cap, batch.prefix_len, batch.tokens,
                   batch.parents, batch.q, batch.u, w.T, w.top_p, w.top_k, outs)
     torch.cuda.synchronize()
+    del Wg  # the packed copy (if any) is no longer read
     log("verify_tree done")
     ho = {k: (host(t) if t is not None else None) for k, t in outs.items()}
     if verifier is None:

@@ -29,7 +29,8 @@ def test_struct_layouts_match_the_header():
     # sizes of the plain structs as laid out by the C compiler on x86-64
     assert ctypes.sizeof(A.ModelDesc) == 40
     assert ctypes.sizeof(A.LayerWeights) == 48
-    assert ctypes.sizeof(A.Weights) == 32
+    assert ctypes.sizeof(A.Weights) == 40
+    assert A.Weights.layout.offset == 32
     assert ctypes.sizeof(A.KVCache) == 32
     assert ctypes.sizeof(A.Params) == 12
     assert ctypes.sizeof(A.Outputs) == 96
@@ -67,3 +68,25 @@ def test_commit_rejects_new_prefix_len_aliasing_prefix_len():
     rc = lib.acespec_commit_kv(None, ctypes.byref(kv), 0x3000, 0x4000, None, B, N, base + 16,
                                None)
     assert rc == A.ACESPEC_EINVAL and "ctx is NULL" in A.acespec_last_error()
+
+
+def test_pack_weight_rejects_bad_shapes_and_overlap_before_launching():
+    """acespec_pack_weight checks its arguments before anything is enqueued (the pointers
+    below are never dereferenced)."""
+    lib = A.load()
+    src, dst = 0x7F0000100000, 0x7F0000900000
+    for rows, cols in ((0, 64), (15, 64), (16, 48), (24, 64), (16, 0)):
+        assert lib.acespec_pack_weight(src, dst, rows, cols, None) == A.ACESPEC_EINVAL
+        assert "multiple of 16" in A.acespec_last_error()
+    assert lib.acespec_pack_weight(None, dst, 16, 32, None) == A.ACESPEC_EINVAL
+    assert lib.acespec_pack_weight(src, None, 16, 32, None) == A.ACESPEC_EINVAL
+    # dst starting inside src's 16 x 32 x 2 = 1024 bytes
+    assert lib.acespec_pack_weight(src, src + 512, 16, 32, None) == A.ACESPEC_EINVAL
+    assert "overlap" in A.acespec_last_error()
+
+
+def test_header_declares_the_weight_layouts():
+    src = open(os.path.join(ROOT, "include", "acespec.h")).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"\b(ACESPEC_LAYOUT_[A-Z]+)\s*=\s*(\d+)", src))
+    assert enum == {"ACESPEC_LAYOUT_ROWS": A.ACESPEC_LAYOUT_ROWS,
+                    "ACESPEC_LAYOUT_PACKED": A.ACESPEC_LAYOUT_PACKED}

@@ -65,6 +65,44 @@ def test_tree_small_bf16(variant):
     _check_tree(run, tol=2e-2)
 
 
+@pytest.mark.parametrize("variant", [
+    dict(),
+    dict(hd=128, H=4, Hkv=1, d=256, tree="chain_sib", depth=6, sib=2, V=4112),
+    dict(hd=64, H=16, Hkv=2, d=256, tree="chain_sib", depth=8, sib=7, B=2, S=300, top_k=32,
+         V=4096),
+])
+def test_tree_small_bf16_packed_weights(variant):
+    """The same forward with the dense matrices in the packed layout
+    (acespec_pack_weight): every GEMM takes its weight operands straight from the packed
+    copy."""
+    w = small_bf16(**dict(dict(V=5008), **variant))
+    run = hz.run_tree(w, packed=True)
+    _check_tree(run, tol=2e-2)
+
+
+def test_pack_weight_layout_matches_its_definition():
+    """acespec_pack_weight against the layout written out on the host: 16-byte unit
+    u = (nb * cols/32 + kt) * 64 + l holds row nb*16 + l%16, columns kt*32 + (l/16)*8 .. +8,
+    widened to fp16."""
+    from paper_2609_02514_amd.acespec import Verifier, acespec_pack_weight
+    rows, cols = 48, 96
+    g = torch.Generator().manual_seed(7)
+    src = (torch.randn(rows, cols, generator=g) * 0.05).to(torch.bfloat16)
+    dst = torch.empty(rows * cols, dtype=torch.float16, device="cuda")
+    srcd = src.cuda()
+    acespec_pack_weight(srcd.data_ptr(), dst.data_ptr(), rows, cols, Verifier._stream())
+    torch.cuda.synchronize()
+    got = dst.cpu().numpy().reshape(rows // 16, cols // 32, 64, 8)
+    ref = np.empty_like(got)
+    s16 = src.to(torch.float16).numpy()
+    for nb in range(rows // 16):
+        for kt in range(cols // 32):
+            for l in range(64):
+                r, c = nb * 16 + l % 16, kt * 32 + (l // 16) * 8
+                ref[nb, kt, l] = s16[r, c:c + 8]
+    assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+
+
 def test_tree_empty_tree_and_long_ragged_prefix():
     """N = 0 (root only: bonus and top-k only) and prefixes that end mid-chunk."""
     w = small_bf16(tree="chain", depth=0, B=5, S=1000, ragged=True)
@@ -78,7 +116,9 @@ def test_tree_empty_tree_and_long_ragged_prefix():
 def test_tree_1b_full_size(seed):
     """1B-class workload at full size, all 16 sessions through the oracle's forward."""
     w = synth.get("1b-bf16")
-    run = hz.run_tree(w, seed=seed)
+    # even seeds with packed weights (the benchmark's layout), odd ones row-major
+    packed = (seed - w.seed_base) // 100 % 2 == 0
+    run = hz.run_tree(w, seed=seed, packed=packed)
     _check_tree(run, tol=2e-2)
 
 
@@ -89,7 +129,8 @@ def test_tree_8b_full_size(seed):
     batch, decisions on all 64 sessions' 1088 rows."""
     w = synth.get("8b-bf16")
     i = (seed - w.seed_base) // 100
-    run = hz.run_tree(w, seed=seed, sessions=[5 + i, 21 + i, 37 + i, 63 - i])
+    run = hz.run_tree(w, seed=seed, sessions=[5 + i, 21 + i, 37 + i, 63 - i],
+                      packed=i % 2 == 0)
     _check_tree(run, tol=2e-2)
 
 
@@ -110,7 +151,7 @@ def test_tree_8b_long_wide(seed):
     w = synth.get("8b-long-wide")
     i = (seed - w.seed_base) // 100
     sessions = list(range(8)) if i == 0 else [2 * i, 7 - i]
-    run = hz.run_tree(w, seed=seed, sessions=sessions)
+    run = hz.run_tree(w, seed=seed, sessions=sessions, packed=i % 2 == 0)
     _check_tree(run, tol=2e-2)
 
 
@@ -122,7 +163,7 @@ def test_tree_paper_scale_widths(name):
     runs the launch configuration of the full-depth model (depth changes only the layer
     loop), and the float64 oracle stays within seconds per session."""
     w = synth.get(name).scaled(L=2)
-    run = hz.run_tree(w, sessions=[11, 50])
+    run = hz.run_tree(w, sessions=[11, 50], packed=name == "70b-bf16")
     _check_tree(run, tol=2e-2)
 
 
@@ -132,7 +173,7 @@ def test_tree_70b_widths_64_node_tree():
     64-node tree: 520 query rows per kv head, more than one attention workgroup holds."""
     w = synth.get("70b-bf16").scaled(L=2, B=4, S=1024, tree="chain_sib", depth=8, sib=7,
                                      top_k=64, T=1.0, q_T=1.0, name="70b-wide")
-    run = hz.run_tree(w, sessions=[1, 3])
+    run = hz.run_tree(w, sessions=[1, 3], packed=True)
     _check_tree(run, tol=2e-2)
 
 
