@@ -701,7 +701,6 @@ constexpr GemmVariant kVariants[] = {
     {2, 4, 8, 4, 4, 1, 32, 1},  // 6: 256 x 256, 8 waves of 128 x 64, 64 KB ring, 1 WG per CU
     {2, 2, 4, 4, 4, 2, 32, 1},  // 7: 128 x 128, 4 waves of 64 x 64, 32 KB ring, 2 WGs per CU
     {2, 2, 9, 2, 4, 1, 32, 1},  // 8: 288 x 64, 4 waves of 144 x 32, 72 KB ring, 1 WG per CU
-    {2, 4, 4, 4, 4, 1, 32, 1},  // 9: 128 x 256, 8 waves of 64 x 64, 32 KB ring, 1 WG per CU
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -771,7 +770,7 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
                 float *tmax = nullptr) {
   switch (var) {
 #define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax); break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8)
 #undef CASE
     default: break;
   }
@@ -873,7 +872,7 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
     launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
     break;                                                                                  \
   }
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8)
 #undef CASE
     default: return hipErrorInvalidValue;
   }
@@ -937,14 +936,15 @@ template <>
 hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, int K,
                                       float *qkv, const RopeOut<bf16> &ro, const TreeMeta &meta,
                                       int B, const GemmAux &aux, hipStream_t s) {
-  // packed weights: 128 x 256 tiles of eight 64 x 64 waves, kept whole when they fill most
-  // CUs, so the RoPE and cache write stay in the epilogue
-  const int var = aux.packed ? (M <= 384 ? 7 : 9) : pick_variant(EPI_F32, M, N, K, 0);
+  // packed weights: 128 x 256 tiles kept whole when they fill most CUs, so the RoPE and
+  // cache write stay in the epilogue (measured level with the separate RoPE kernel after
+  // a split product, and with eight 64 x 64 waves a tile)
+  const int var = aux.packed ? (M <= 384 ? 7 : 5) : pick_variant(EPI_F32, M, N, K, 0);
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
   SplitPlan sp = plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
-  if (aux.packed && 4 * mt * nt >= 3 * aux.cus * v.occ) sp = SplitPlan{mt * nt, 1};
+  if (aux.packed && 4 * mt * nt >= 3 * aux.cus) sp = SplitPlan{mt * nt, 1};
   if (sp.tsplit == 1 && tbn % ro.hd == 0 && N == (ro.H + 2 * ro.Hkv) * ro.hd) {
     launch_epi<EPI_QKV_ROPE, bf16>(var, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
                                    sp, ro);
