@@ -330,7 +330,7 @@ def calibrate(reps=5):
 
     ms_copy = timed(lambda: lib.acespec_calib_copy(src.data_ptr(), dst.data_ptr(), nbytes,
                                                    cus * 16, stream.cuda_stream))
-    rblocks = cus * 8
+    rblocks = cus * 32
     rout = torch.empty(rblocks * 4, dtype=torch.float32, device="cuda")
     ms_read = timed(lambda: lib.acespec_calib_read(src.data_ptr(), rout.data_ptr(), nbytes,
                                                    rblocks, stream.cuda_stream))
@@ -343,7 +343,7 @@ def calibrate(reps=5):
             "mfma_f16_loop_tflops": round(flops / (ms_mfma / 1e3) / 1e12, 1),
             "method": (f"median of {reps} HIP-event-timed runs: a 1 GiB device copy "
                        f"(16-byte loads and stores, read + write bytes counted), a 1 GiB "
-                       f"streaming read (four 16-byte loads in flight a thread), and "
+                       f"streaming read (eight nontemporal 16-byte loads in flight a thread), and "
                        f"{blocks} workgroups x 4 waves x {iters} x 16 MFMAs 16x16x32 f16 on "
                        f"random operands generated in registers")}
 

@@ -593,8 +593,10 @@ __global__ __launch_bounds__(VT, 6) void vocab_verify_kernel(acespec::VocabArgs 
   for (int u = 0; u < VU; ++u) {
     const int id0 = (s0 + u * NWV) * SEG + lane * 4;
     const int ld = id0 < V ? id0 : V - 4;
-    z4u[u] = *(const float4 *)(z + ld);
-    q4u[u] = resid ? *(const float4 *)(q + ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+    // last pass over the row and its draft q: streamed past L2 and the MALL (the
+    // earlier passes keep the default policy, so their re-reads may hit the MALL)
+    z4u[u] = ld_stream(z + ld);
+    q4u[u] = resid ? ld_stream(q + ld) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
 #pragma unroll
   for (int u = 0; u < VU; ++u) {
