@@ -82,14 +82,20 @@ constexpr int epi_smem(int epi, int tbm, int tbn, int wnn) {
 //   activations go through LDS.  A packed fragment is 1 KB of contiguous memory, so these
 //   loads are as cheap for the address unit as the row-contiguous DMA, while LDS carries a
 //   third of the bytes (no weight rows written, no weight fragments read) and no widening
-//   instructions run.  KSS = 32 only.
+//   instructions run.  KSS = 32.
+// PK = 2: as PK = 1 with twice the waves, the tile's k-steps split between two wave
+//   groups (even and odd 32-wide steps of each 64-wide stage, 128-byte activation rows),
+//   whose accumulators are summed through LDS before the epilogue: two waves a SIMD for
+//   a product with fewer tiles than CUs, without fp32 partials in memory (QKV + RoPE
+//   epilogue only).  KSS = 64.
 template <int EPI, typename TB, int WMN, int WNN, int WTM, int WTN, int NST, int OCC, int KSS,
           int PK>
-__global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
+__global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_f16w_kernel(
     const f16 *__restrict__ A, const void *__restrict__ W, int M, int N, int K,
     f16 *__restrict__ out, float *__restrict__ outf, float *__restrict__ part, int mt, int nt,
     int full, int tsplit, acespec::RopeOut<TB> ro, float *__restrict__ tmax) {
-  constexpr int NW = WMN * WNN;
+  constexpr int KG = PK == 2 ? 2 : 1;  // wave groups splitting each stage's k-steps
+  constexpr int NW = WMN * WNN * KG;
   constexpr int TBM = WMN * WTM * 16, TBN = WNN * WTN * 16;
   constexpr int ROWB = KSS * 2, PIECES = KSS / 8, ROWS_PER_BLK = 1024 / ROWB;
   constexpr int A_BYTES = TBM * ROWB, B_BYTES = PK ? 0 : TBN * ROWB;
@@ -104,10 +110,13 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   constexpr int F = KSUB * WTM;             // A fragments per stage, in use order
   static_assert(A_BLKS * 1024 == A_BYTES && B_DMA * 1024 * NW == B_BYTES, "DMA split");
   static_assert(F >= 4 && NST >= 3, "pipeline shape");
-  static_assert(!PK || KSS == 32, "packed weights come in 32-wide k steps");
+  static_assert(!PK || KSS == 32 * KG, "packed weights come in 32-wide k steps, one a group");
+  static_assert(KG == 1 || EPI == acespec::EPI_QKV_ROPE, "split wave groups: QKV epilogue only");
   constexpr int HALF = WTN / 2;  // SwiGLU: gate blocks, then the matching up blocks
   constexpr int RING = NST * STAGE_BYTES, EPI_SM = epi_smem(EPI, TBM, TBN, WNN);
-  __shared__ __attribute__((aligned(1024))) char smem[RING > EPI_SM ? RING : EPI_SM];
+  constexpr int RED = KG > 1 ? WMN * WNN * WTM * WTN * 4 * 64 * 4 : 0;  // group-sum buffer
+  constexpr int SM1 = RING > EPI_SM ? RING : EPI_SM;
+  __shared__ __attribute__((aligned(1024))) char smem[SM1 > RED ? SM1 : RED];
   typedef typename Vec8<TB>::type tbx8;
 
   // Units: `full` whole tiles, then tsplit k-slices of each remaining tile (their partial
@@ -136,7 +145,8 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   const int nk = kt1 - kt0;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = w / WNN, wn = w - wm * WNN;
+  const int kg = w / (WMN * WNN), wl = w - kg * (WMN * WNN);  // k group, wave in the group
+  const int wm = wl / WNN, wn = wl - wm * WNN;
   const int lr = lane & 15, lk = lane >> 4;
 
   // DMA sources: block j of an operand covers tile rows ROWS_PER_BLK*j ..; lane l lands at
@@ -186,7 +196,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
         c = tn * TBN + wn * WTN * 16 + j * 16;
         base = c < N ? c : N - 16;
       }
-      pkw[j] = (const f16x8 *)W + (size_t)(base >> 4) * KT * 64 + lane;
+      pkw[j] = (const f16x8 *)W + (size_t)(base >> 4) * (K / 32) * 64 + lane;
     }
   }
   auto issue = [&](int kt, int stage) {
@@ -231,13 +241,18 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
     // after the barrier every wave's have, and every wave is done with slot i - 1, which
     // the loads of step i + NST - 1 then refill.
     constexpr int L_VM = A_DMA + WTN;
-    f16x8 rb[NST][WTN], fa[F];
+    constexpr int FW = WTM;  // A fragments of this wave's k-step
+    f16x8 rb[NST][WTN], fa[FW];
+    int aok[FW];  // this group's 16-byte pieces of the stage's rows
+#pragma unroll
+    for (int f = 0; f < FW; ++f)
+      aok[f] = piece_off<ROWB>(wm * WTM * 16 + f * 16 + lr, kg * 4 + lk);
 #pragma unroll
     for (int p = 0; p < NST - 1; ++p) {
       const int kt = kt0 + (p < nk ? p : nk - 1);
       issue(kt, p);
 #pragma unroll
-      for (int j = 0; j < WTN; ++j) rb[p][j] = pkw[j][(size_t)kt * 64];
+      for (int j = 0; j < WTN; ++j) rb[p][j] = pkw[j][(size_t)(kt * KG + kg) * 64];
     }
     for (int i0 = 0; i0 < nk; i0 += NST) {
 #pragma unroll
@@ -248,14 +263,15 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
         const int kn = kt0 + (i0 + u + NST - 1 < nk ? i0 + u + NST - 1 : nk - 1);
         issue(kn, (u + NST - 1) % NST);
 #pragma unroll
-        for (int j = 0; j < WTN; ++j) rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)kn * 64];
+        for (int j = 0; j < WTN; ++j)
+          rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)(kn * KG + kg) * 64];
         const char *sc = smem + u * STAGE_BYTES;
-        fa[0] = *(const f16x8 *)(sc + aoff[0]);
-        fa[1] = *(const f16x8 *)(sc + aoff[1]);
-        fa[2] = *(const f16x8 *)(sc + aoff[2]);
+        fa[0] = *(const f16x8 *)(sc + aok[0]);
+        fa[1] = *(const f16x8 *)(sc + aok[1]);
+        fa[2] = *(const f16x8 *)(sc + aok[2]);
 #pragma unroll
-        for (int f = 0; f < F; ++f) {
-          if (f + 3 < F) fa[f + 3] = *(const f16x8 *)(sc + aoff[f + 3]);
+        for (int f = 0; f < FW; ++f) {
+          if (f + 3 < FW) fa[f + 3] = *(const f16x8 *)(sc + aok[f + 3]);
           SCHED_FENCE();
 #pragma unroll
           for (int j = 0; j < WTN; ++j)
@@ -315,6 +331,30 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
   }
   // No LDS DMA may still be writing when the workgroup's LDS is released.
   wait_vmcnt<0>();
+  if constexpr (KG > 1) {
+    // the wave groups' sums of their k-steps: group 1 hands its blocks to group 0
+    __syncthreads();  // every wave is past the ring
+    float *red = (float *)smem;
+    if (kg == 1) {
+#pragma unroll
+      for (int ii = 0; ii < WTM; ++ii)
+#pragma unroll
+        for (int j = 0; j < WTN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            red[(((wl * WTM + ii) * WTN + j) * 4 + e) * 64 + lane] = acc[ii][j][e];
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int ii = 0; ii < WTM; ++ii)
+#pragma unroll
+        for (int j = 0; j < WTN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            acc[ii][j][e] += red[(((wl * WTM + ii) * WTN + j) * 4 + e) * 64 + lane];
+    }
+  }
 
   if constexpr (EPI == acespec::EPI_QKV_ROPE) {
     // QKV projection (never sliced along K here): the fp32 tile goes through LDS in
@@ -343,7 +383,7 @@ __global__ __launch_bounds__(WMN * WNN * 64, OCC) void gemm_f16w_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int lrow = wm * WTM * 16 + ii * 16 + lk * 4 + e - c0;
-          if (lrow < 0 || lrow >= CR) continue;
+          if (lrow < 0 || lrow >= CR || kg != 0) continue;  // group 0 holds the sums
 #pragma unroll
           for (int j = 0; j < WTN; ++j) st[lrow * SP + wn * WTN * 16 + j * 16 + lr] = acc[ii][j][e];
         }
@@ -701,6 +741,7 @@ constexpr GemmVariant kVariants[] = {
     {2, 4, 8, 4, 4, 1, 32, 1},  // 6: 256 x 256, 8 waves of 128 x 64, 64 KB ring, 1 WG per CU
     {2, 2, 4, 4, 4, 2, 32, 1},  // 7: 128 x 128, 4 waves of 64 x 64, 32 KB ring, 2 WGs per CU
     {2, 2, 9, 2, 4, 1, 32, 1},  // 8: 288 x 64, 4 waves of 144 x 32, 72 KB ring, 1 WG per CU
+    {1, 4, 8, 4, 4, 1, 64, 2},  // 9: 128 x 256, two groups of 4 waves of 128 x 64 splitting k
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -751,7 +792,7 @@ void launch_variant(hipStream_t s, const f16 *A, const TB *W, int M, int N, int 
   const int units = sp.full + (tiles - sp.full) * sp.tsplit;
   hipLaunchKernelGGL(
         (gemm_f16w_kernel<EPI, TB, v.wmn, v.wnn, v.wtm, v.wtn, v.nst, v.occ, v.kss, v.pk>),
-        dim3(units), dim3(v.wmn * v.wnn * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
+        dim3(units), dim3(v.wmn * v.wnn * (v.pk == 2 ? 2 : 1) * 64), 0, s, A, W, M, N, K, out, outf, part, mt, nt,
         sp.full, sp.tsplit, ro, tmax);
   if (sp.tsplit > 1) {
     const int nsplit_tiles = tiles - sp.full;
@@ -769,8 +810,12 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
                 const acespec::RopeOut<TB> &ro = acespec::RopeOut<TB>{},
                 float *tmax = nullptr) {
   switch (var) {
-#define CASE(V) case V: launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax); break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8)
+#define CASE(V)                                                                             \
+  case V:                                                                                   \
+    if constexpr (kVariants[V].pk != 2 || EPI == acespec::EPI_QKV_ROPE)                     \
+      launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax);  \
+    break;
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
 #undef CASE
     default: break;
   }
@@ -939,13 +984,24 @@ hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N,
   // packed weights: 128 x 256 tiles kept whole when they fill most CUs, so the RoPE and
   // cache write stay in the epilogue (measured level with the separate RoPE kernel after
   // a split product, and with eight 64 x 64 waves a tile)
+  const bool fusable = N == (ro.H + 2 * ro.Hkv) * ro.hd;
+  if (aux.packed && M >= 1024 && fusable && 256 % ro.hd == 0) {
+    // ~1k rows or more: 128 x 256 tiles whole, each with two wave groups splitting its
+    // k-steps (two waves a SIMD on the ~200 tiles), RoPE and cache write in the epilogue
+    constexpr GemmVariant g = kVariants[9];
+    const int mt = (M + g.wtm * 16 * g.wmn - 1) / (g.wtm * 16 * g.wmn);
+    const int nt = (N + g.wtn * 16 * g.wnn - 1) / (g.wtn * 16 * g.wnn);
+    launch_epi<EPI_QKV_ROPE, bf16>(9, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
+                                   SplitPlan{mt * nt, 1}, ro);
+    return hipGetLastError();
+  }
   const int var = aux.packed ? (M <= 384 ? 7 : 5) : pick_variant(EPI_F32, M, N, K, 0);
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
   SplitPlan sp = plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
   if (aux.packed && 4 * mt * nt >= 3 * aux.cus) sp = SplitPlan{mt * nt, 1};
-  if (sp.tsplit == 1 && tbn % ro.hd == 0 && N == (ro.H + 2 * ro.Hkv) * ro.hd) {
+  if (sp.tsplit == 1 && tbn % ro.hd == 0 && fusable) {
     launch_epi<EPI_QKV_ROPE, bf16>(var, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
                                    sp, ro);
     return hipGetLastError();
