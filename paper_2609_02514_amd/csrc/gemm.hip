@@ -742,6 +742,7 @@ constexpr GemmVariant kVariants[] = {
     {2, 2, 4, 4, 4, 2, 32, 1},  // 7: 128 x 128, 4 waves of 64 x 64, 32 KB ring, 2 WGs per CU
     {2, 2, 9, 2, 4, 1, 32, 1},  // 8: 288 x 64, 4 waves of 144 x 32, 72 KB ring, 1 WG per CU
     {1, 4, 8, 4, 4, 1, 64, 2},  // 9: 128 x 256, two groups of 4 waves of 128 x 64 splitting k
+    {2, 2, 4, 4, 4, 1, 64, 2},  // 10: 128 x 128, two groups of 4 waves of 64 x 64 splitting k
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -815,7 +816,7 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
     if constexpr (kVariants[V].pk != 2 || EPI == acespec::EPI_QKV_ROPE)                     \
       launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax);  \
     break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9) CASE(10)
 #undef CASE
     default: break;
   }
@@ -985,15 +986,19 @@ hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N,
   // cache write stay in the epilogue (measured level with the separate RoPE kernel after
   // a split product, and with eight 64 x 64 waves a tile)
   const bool fusable = N == (ro.H + 2 * ro.Hkv) * ro.hd;
-  if (aux.packed && M >= 1024 && fusable && 256 % ro.hd == 0) {
-    // ~1k rows or more: 128 x 256 tiles whole, each with two wave groups splitting its
-    // k-steps (two waves a SIMD on the ~200 tiles), RoPE and cache write in the epilogue
-    constexpr GemmVariant g = kVariants[9];
+  if (aux.packed && M > 384 && fusable && 128 % ro.hd == 0) {
+    // tiles kept whole, each with two wave groups splitting its k-steps (two waves a SIMD
+    // with about one tile a CU), RoPE and cache write in the epilogue: 128 x 256 tiles from
+    // ~1k rows, 128 x 128 below
+    const int gv = M >= 1024 ? 9 : 10;
+    const GemmVariant g = kVariants[gv];
     const int mt = (M + g.wtm * 16 * g.wmn - 1) / (g.wtm * 16 * g.wmn);
     const int nt = (N + g.wtn * 16 * g.wnn - 1) / (g.wtn * 16 * g.wnn);
-    launch_epi<EPI_QKV_ROPE, bf16>(9, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
-                                   SplitPlan{mt * nt, 1}, ro);
-    return hipGetLastError();
+    if (4 * mt * nt >= 3 * aux.cus) {
+      launch_epi<EPI_QKV_ROPE, bf16>(gv, s, A, W, M, N, K, nullptr, nullptr, aux.part, mt, nt,
+                                     SplitPlan{mt * nt, 1}, ro);
+      return hipGetLastError();
+    }
   }
   const int var = aux.packed ? (M <= 384 ? 7 : 5) : pick_variant(EPI_F32, M, N, K, 0);
   const GemmVariant v = kVariants[var];
