@@ -505,7 +505,10 @@ def main():
         # does this when it loads the model); the row-major W stays for the oracle
         if args.layout == "auto":
             args.layout = "packed" if B * n1 >= 512 and w.dtype == "bf16" else "rows"
-        Wg = v.pack_weights(W) if args.layout == "packed" else W
+        # (without the oracle's CPU baseline nothing reads the row-major copy again: it is
+        # released as it is packed, which lets the 70B-class shape fit one GPU packed)
+        Wg = (v.pack_weights(W, drop_source=args.no_cpu_baseline) if args.layout == "packed"
+              else W)
         torch.cuda.synchronize()
         ws = v.weights_struct(Wg)
         outs = v.alloc_outputs(B * n1, B, n1, w.top_k, w.V, "cuda", False)

@@ -247,10 +247,12 @@ class Verifier:
 
     DENSE = ("wqkv", "wo", "w_gate_up", "w_down")
 
-    def pack_weights(self, W):
+    def pack_weights(self, W, drop_source=False):
         """A copy of W whose dense matrices (the DENSE ones of every layer and the LM head)
         are in the packed layout (acespec_pack_weight); the embedding and the norm gains
-        are shared with W.  The result carries `packed = True` for weights_struct."""
+        are shared with W.  The result carries `packed = True` for weights_struct.
+        drop_source: release each row-major matrix of W once it is packed (W's entries
+        become None), so that a model only slightly smaller than the device fits."""
         import copy
         import torch
 
@@ -260,8 +262,15 @@ class Verifier:
             return out
 
         P = copy.copy(W)
-        P.layers = [dict(lw, **{k: pk(lw[k]) for k in self.DENSE}) for lw in W.layers]
+        P.layers = []
+        for lw in W.layers:
+            P.layers.append(dict(lw, **{k: pk(lw[k]) for k in self.DENSE}))
+            if drop_source:
+                for k in self.DENSE:
+                    lw[k] = None
         P.lm_head = pk(W.lm_head)
+        if drop_source:
+            W.lm_head = None
         P.packed = True
         return P
 
