@@ -420,8 +420,8 @@ def main():
     ap.add_argument("--workload", default="8b-bf16")
     ap.add_argument("--layout", choices=("auto", "packed", "rows"), default="auto",
                     help="dense weight matrices of the tree step: packed fragment order "
-                         "(acespec_pack_weight) or row-major bf16; auto = packed for steps "
-                         "of at least 512 rows, where it measures faster, else row-major")
+                         "(acespec_pack_weight) or row-major bf16; auto = packed for bf16 "
+                         "models (measured faster from 272 to 4096 rows), row-major for fp32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step into a HIP graph (stream capture) and time its "
@@ -504,7 +504,7 @@ def main():
         # packed: the dense matrices re-laid out once, before anything is timed (a server
         # does this when it loads the model); the row-major W stays for the oracle
         if args.layout == "auto":
-            args.layout = "packed" if B * n1 >= 512 and w.dtype == "bf16" else "rows"
+            args.layout = "packed" if w.dtype == "bf16" else "rows"
         # (without the oracle's CPU baseline nothing reads the row-major copy again: it is
         # released as it is packed, which lets the 70B-class shape fit one GPU packed)
         Wg = (v.pack_weights(W, drop_source=args.no_cpu_baseline) if args.layout == "packed"

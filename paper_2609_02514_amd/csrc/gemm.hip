@@ -254,32 +254,40 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
 #pragma unroll
       for (int j = 0; j < WTN; ++j) rb[p][j] = pkw[j][(size_t)(kt * KG + kg) * 64];
     }
-    for (int i0 = 0; i0 < nk; i0 += NST) {
+    // One k-step (i = the step, u = i % NST, a constant once the callers are unrolled).
+    auto step = [&](int i, int u) {
+      wait_vmcnt<(NST - 2) * L_VM>();
+      __builtin_amdgcn_s_barrier();
+      const int kn = kt0 + (i + NST - 1 < nk ? i + NST - 1 : nk - 1);
+      issue(kn, (u + NST - 1) % NST);
 #pragma unroll
-      for (int u = 0; u < NST; ++u) {
-        if (i0 + u >= nk) break;
-        wait_vmcnt<(NST - 2) * L_VM>();
-        __builtin_amdgcn_s_barrier();
-        const int kn = kt0 + (i0 + u + NST - 1 < nk ? i0 + u + NST - 1 : nk - 1);
-        issue(kn, (u + NST - 1) % NST);
+      for (int j = 0; j < WTN; ++j)
+        rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)(kn * KG + kg) * 64];
+      const char *sc = smem + u * STAGE_BYTES;
+      fa[0] = *(const f16x8 *)(sc + aok[0]);
+      fa[1] = *(const f16x8 *)(sc + aok[1]);
+      fa[2] = *(const f16x8 *)(sc + aok[2]);
+#pragma unroll
+      for (int f = 0; f < FW; ++f) {
+        if (f + 3 < FW) fa[f + 3] = *(const f16x8 *)(sc + aok[f + 3]);
+        SCHED_FENCE();
 #pragma unroll
         for (int j = 0; j < WTN; ++j)
-          rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)(kn * KG + kg) * 64];
-        const char *sc = smem + u * STAGE_BYTES;
-        fa[0] = *(const f16x8 *)(sc + aok[0]);
-        fa[1] = *(const f16x8 *)(sc + aok[1]);
-        fa[2] = *(const f16x8 *)(sc + aok[2]);
-#pragma unroll
-        for (int f = 0; f < FW; ++f) {
-          if (f + 3 < FW) fa[f + 3] = *(const f16x8 *)(sc + aok[f + 3]);
-          SCHED_FENCE();
-#pragma unroll
-          for (int j = 0; j < WTN; ++j)
-            acc[f][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[f], rb[u][j], acc[f][j], 0, 0, 0);
-          SCHED_FENCE();
-        }
+          acc[f][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[f], rb[u][j], acc[f][j], 0, 0, 0);
+        SCHED_FENCE();
       }
+    };
+    // Whole rounds of NST steps run as straight-line code: with a conditional exit between
+    // the steps the compiler moves each step's weight loads down to the step that reads
+    // them, so their latency is no longer covered by the NST - 1 steps in between.
+    int i0 = 0;
+    for (; i0 + NST <= nk; i0 += NST) {
+#pragma unroll
+      for (int u = 0; u < NST; ++u) step(i0 + u, u);
     }
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u)
+      if (i0 + u < nk) step(i0 + u, u);
   } else {
   for (int p = 0; p < NST - 1; ++p) issue(kt0 + (p < nk ? p : nk - 1), p);
   wait_vmcnt<(NST - 2) * L_DMA>();  // stage 0 landed for this wave
