@@ -125,6 +125,12 @@ template <int VM> AS_DEVICE void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Waits until no LDS or scalar memory access of this wave is outstanding.  Before a loop
+// it spares the loop's LDS reads a full wait on every iteration: the compiler merges the
+// counter state of the code before the loop (scalar loads of kernel arguments, which
+// complete out of order) into the loop head, where it then cannot count LDS reads.
+AS_DEVICE void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt((0xF) | (0x3 << 14) | (0x7 << 4)); }
+
 // Workgroup barrier that orders LDS accesses only: unlike __syncthreads() it does not
 // drain outstanding global loads, so DMA into other stages stays in flight.
 AS_DEVICE void lds_barrier() {

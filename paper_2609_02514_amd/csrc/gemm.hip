@@ -259,10 +259,6 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
       wait_vmcnt<(NST - 2) * L_VM>();
       __builtin_amdgcn_s_barrier();
       const int kn = kt0 + (i + NST - 1 < nk ? i + NST - 1 : nk - 1);
-      issue(kn, (u + NST - 1) % NST);
-#pragma unroll
-      for (int j = 0; j < WTN; ++j)
-        rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)(kn * KG + kg) * 64];
       const char *sc = smem + u * STAGE_BYTES;
       fa[0] = *(const f16x8 *)(sc + aok[0]);
       fa[1] = *(const f16x8 *)(sc + aok[1]);
@@ -275,12 +271,19 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
         for (int j = 0; j < WTN; ++j)
           acc[f][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[f], rb[u][j], acc[f][j], 0, 0, 0);
         SCHED_FENCE();
+        if (f == 0) {
+          issue(kn, (u + NST - 1) % NST);
+#pragma unroll
+          for (int j = 0; j < WTN; ++j)
+            rb[(u + NST - 1) % NST][j] = pkw[j][(size_t)(kn * KG + kg) * 64];
+        }
       }
     };
     // Whole rounds of NST steps run as straight-line code: with a conditional exit between
     // the steps the compiler moves each step's weight loads down to the step that reads
     // them, so their latency is no longer covered by the NST - 1 steps in between.
     int i0 = 0;
+    wait_lgkmcnt0();
     for (; i0 + NST <= nk; i0 += NST) {
 #pragma unroll
       for (int u = 0; u < NST; ++u) step(i0 + u, u);
@@ -727,10 +730,11 @@ using acespec::EPI_F32;
 using acespec::EPI_F32_MAX;
 
 // Tilings: {waves M, waves N, wave tile M / 16, wave tile N / 16, stages, WGs per CU,
-// k per stage}.  Measured on MI355X against the verify-step shapes.  Tried and slower on
-// every shape here: ping-pong pairs of waves per SIMD (one issuing 32 x 32 MFMAs while
-// the other loads), deeper rings (5-8 stages) at one workgroup per CU, with 64 x 64 wave
-// tiles or 128 x 512 block tiles, 128 x 128 tiles with 64-wide k stages, fp16 weights
+// k per stage, weight layout}.  Measured on MI355X against the verify-step shapes.  Tried
+// and slower on every shape here with row-major weights: ping-pong pairs of waves per SIMD
+// (one issuing 32 x 32 MFMAs while the other loads), deeper rings (5-8 stages) at one
+// workgroup per CU, with 64 x 64 wave tiles or 128 x 512 block tiles (with packed weights
+// 128 x 512 tiles are the fastest), 128 x 128 tiles with 64-wide k stages, fp16 weights
 // (which only removes the in-register widening, worth 3-8 %), and weights and
 // activations pre-packed into 1 KB tile blocks (contiguous DMA; 2-9 %), 256 x 128 tiles,
 // and 256 x 256 tiles on 32 x 32 MFMAs with one wave per SIMD (128 x 128 wave tiles: the
@@ -751,6 +755,8 @@ constexpr GemmVariant kVariants[] = {
     {2, 2, 9, 2, 4, 1, 32, 1},  // 8: 288 x 64, 4 waves of 144 x 32, 72 KB ring, 1 WG per CU
     {1, 4, 8, 4, 4, 1, 64, 2},  // 9: 128 x 256, two groups of 4 waves of 128 x 64 splitting k
     {2, 2, 4, 4, 4, 1, 64, 2},  // 10: 128 x 128, two groups of 4 waves of 64 x 64 splitting k
+    {1, 8, 8, 4, 4, 1, 32, 1},  // 11: 128 x 512, 8 waves of 128 x 64, 32 KB ring, 1 WG per CU
+    {1, 8, 4, 4, 4, 1, 32, 1},  // 12: 64 x 512, 8 waves of 64 x 64, 16 KB ring, 1 WG per CU
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -824,7 +830,7 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
     if constexpr (kVariants[V].pk != 2 || EPI == acespec::EPI_QKV_ROPE)                     \
       launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax);  \
     break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9) CASE(10)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9) CASE(10) CASE(11) CASE(12)
 #undef CASE
     default: break;
   }
@@ -837,15 +843,19 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
 // (for the gate/up product at ~1k rows both tilings measure the same, the 256 x 256 one
 // only with its last round sliced).
 int pick_variant(int epi, int M, int N, int K, int packed) {
-  (void)K;
   if (packed) {
-    // measured on MI355X in the verify steps (272 - 4096 rows): 128 x 256 tiles for most
-    // products; 288 x 64 (gate/up) and 128 x 128 tiles for few-row batches, 256 x 256
-    // (fewer operand bytes per flop) for the residual products of ~1k rows and for
-    // thousands of rows
-    if (M <= 288 && epi == EPI_SWIGLU) return 8;
+    // measured on MI355X in the verify steps (272 - 4096 rows).  What sets these products'
+    // rate is the bytes each CU's address unit moves per k-step: one 512-column tile of
+    // eight waves shares its activation rows across twice the columns of a 256-column
+    // one (40 instead of 48 KB a CU per k-step at 128 rows), so from ~500 rows the
+    // products take 128 x 512 tiles (64 x 512 for the residual product with a short K
+    // at ~520 rows, where 128-row tiles leave most of a last round empty); few-row
+    // batches keep 288 x 64 tiles for the gate/up product and 128 x 128 ones otherwise
+    if (epi == EPI_SWIGLU) return M <= 288 ? 8 : 11;
     if (M <= 384) return 7;
-    if (M >= 2048 || (M >= 1024 && epi == EPI_RESID)) return 6;
+    if (epi == EPI_RESID) return K < 8192 && M <= 640 ? 12 : 11;
+    if (M >= 512 && N >= 16384) return 11;
+    if (M >= 2048) return 6;
     return 5;
   }
   // gate/up with up to 288 rows (a 16-session 1B-class batch: 272): one tile spans every
@@ -926,7 +936,7 @@ hipError_t launch_gemm_resid_norm<bf16, f16>(const f16 *A, const bf16 *W, int M,
     launch_resid_norm_fixup<VV, bf16>(s, aux.part, x, gain, out, M, N, mt, sp.tsplit, eps); \
     break;                                                                                  \
   }
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(11) CASE(12)
 #undef CASE
     default: return hipErrorInvalidValue;
   }
@@ -1046,11 +1056,13 @@ hipError_t launch_lm_head<bf16, f16>(const f16 *A, const bf16 *W, int M, int N, 
   const GemmVariant v = kVariants[var];
   const int tbm = v.wmn * v.wtm * 16, tbn = v.wnn * v.wtn * 16;
   const int mt = (M + tbm - 1) / tbm, nt = (N + tbn - 1) / tbn;
-  const SplitPlan sp =
-      plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
-  if (tile_max == nullptr || (sp.tsplit > 1 && (tbn / 4) > 64))
+  SplitPlan sp = plan_split(M, N, K, v.kss, tbm, tbn, mt * nt, aux.cus, v.occ, aux.part_cap);
+  if (tile_max == nullptr)
     return launch_f16w_variant<bf16>(var, 0, EPI_F32, A, W, M, N, K, nullptr, logits, aux.part,
                                      aux.part_cap, aux.cus, s, aux.packed);
+  // the row maxima of sliced tiles are reduced by tbn / 4 lanes of one wave: wider tiles
+  // stay whole (at most part of a last round idles)
+  if (sp.tsplit > 1 && tbn / 4 > 64) sp = SplitPlan{mt * nt, 1};
   launch_epi<EPI_F32_MAX, bf16>(var, s, A, W, M, N, K, nullptr, logits, aux.part, mt, nt, sp,
                                 RopeOut<bf16>{}, tile_max);
   *ntile = nt;
