@@ -485,6 +485,8 @@ def main():
     W = synth.make_weights(w, "cuda")
     batch = synth.make_batch(w, "cuda")
     v = Verifier.for_workload(w)
+    if args.layout == "auto":
+        args.layout = "packed" if w.dtype == "bf16" else "rows"
     if tail:
         # LM head + vocabulary verify over given hidden states: every row is the parent of
         # one drafted token (acespec_verify_tail); B chains of chain_len rows.
@@ -492,10 +494,13 @@ def main():
         B, n1 = R // w.chain_len, w.chain_len
         P, S_tot = R, 0
         outs = v.alloc_outputs(R, B, n1, w.top_k, w.V, "cuda", False)
+        packed = args.layout == "packed"
+        Wg = v.pack_weights(W, drop_source=args.no_cpu_baseline) if packed else W
+        torch.cuda.synchronize()
 
         def step():
-            v.verify_tail(W.lm_head, None, batch.hidden, batch.draft_tokens, batch.q, batch.u,
-                          w.chain_len, w.T, w.top_p, w.top_k, outs)
+            v.verify_tail(Wg.lm_head, None, batch.hidden, batch.draft_tokens, batch.q, batch.u,
+                          w.chain_len, w.T, w.top_p, w.top_k, outs, packed=packed)
     else:
         B, n1 = batch.tokens.shape
         parents = synth.tree_parents(w)
@@ -503,8 +508,6 @@ def main():
         S_tot = int(batch.prefix_len.sum().item()) + B * n1
         # packed: the dense matrices re-laid out once, before anything is timed (a server
         # does this when it loads the model); the row-major W stays for the oracle
-        if args.layout == "auto":
-            args.layout = "packed" if w.dtype == "bf16" else "rows"
         # (without the oracle's CPU baseline nothing reads the row-major copy again: it is
         # released as it is packed, which lets the 70B-class shape fit one GPU packed)
         Wg = (v.pack_weights(W, drop_source=args.no_cpu_baseline) if args.layout == "packed"
@@ -705,7 +708,8 @@ def main():
         "dtype": "bf16 weights/KV, fp16 activations on f16 MFMA, fp32 accumulate",
         "data": "synthetic (seeded random-init weights, KV prefix, drafted trees, draft q)",
         "config": ({"workload": w.name, "d_model": w.d, "vocab": w.V, "rows": B * n1,
-                    "chain_len": n1, "temperature": w.T, "top_p": w.top_p, "top_k": w.top_k}
+                    "chain_len": n1, "temperature": w.T, "top_p": w.top_p, "top_k": w.top_k,
+                    "weight_layout": args.layout}
                    if tail else
                    {"workload": w.name, "layers": w.L, "d_model": w.d, "heads": w.H,
                     "kv_heads": w.Hkv, "head_dim": w.hd, "d_ff": w.F, "vocab": w.V,

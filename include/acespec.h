@@ -187,7 +187,10 @@ int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *weight
 /* LM head and verification only, over R given hidden states (the last stage of
  * verify_tree on its own).  Each row r is the parent of one drafted token
  * draft_tokens[r]; rows form chains of chain_len consecutive rows (R % chain_len == 0).
- *  lm_head [vocab, d_model], final_norm [d_model] or NULL (no normalisation),
+ *  lm_head [vocab, d_model] in the layout lm_head_layout (ACESPEC_LAYOUT_PACKED: as
+ *          written by acespec_pack_weight, for bf16 models with vocab a multiple of 16;
+ *          another value: ACESPEC_EINVAL, a packed head otherwise ACESPEC_EUNSUPPORTED),
+ *  final_norm [d_model] or NULL (no normalisation),
  *  hidden [R, d_model] in the model dtype, draft_q [R, vocab], uniforms [R, 3].
  * Per row: accept, resample_token, bonus_token, topk_*, acc_prefix_len (leading accepts
  * within its chain, counting the row).  Per chain c: path_len[c] = leading accepts,
@@ -197,8 +200,8 @@ int acespec_verify_tree_scalar_q(acespec_ctx *ctx, const acespec_weights *weight
  * status[c] = OK, EBADTREE (a draft token outside the vocabulary), or EBADDRAFT /
  * ENONFINITE for a row of the chain (without final_norm, hidden values beyond the fp16
  * range of a bf16 model overflow and give ENONFINITE).  path is [R/chain_len, chain_len]. */
-int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
-                        const void *hidden, const int32_t *draft_tokens,
+int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, acespec_layout lm_head_layout,
+                        const void *final_norm, const void *hidden, const int32_t *draft_tokens,
                         const float *draft_q, const float *uniforms, int R, int chain_len,
                         const acespec_params *params, const acespec_outputs *outs,
                         hipStream_t stream);
@@ -218,7 +221,8 @@ int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final
  * device race (serialise them, e.g. on one stream).  Every byte a call reads from the
  * array it has written first, so no clearing is needed between calls. */
 int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_head,
-                                const void *final_norm, const void *hidden,
+                                acespec_layout lm_head_layout, const void *final_norm,
+                                const void *hidden,
                                 const int32_t *draft_tokens, const float *draft_q,
                                 const float *uniforms, int R, int chain_len,
                                 const acespec_params *params, const acespec_outputs *outs,

@@ -85,13 +85,14 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.acespec_verify_tree.restype = C.c_int
     lib.acespec_verify_tree_scalar_q.argtypes = lib.acespec_verify_tree.argtypes
     lib.acespec_verify_tree_scalar_q.restype = C.c_int
-    lib.acespec_verify_tail.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int, C.c_int,
-                                        C.POINTER(Params), C.POINTER(Outputs), C.c_void_p]
+    lib.acespec_verify_tail.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_void_p,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_int, C.c_int, C.POINTER(Params),
+                                        C.POINTER(Outputs), C.c_void_p]
     lib.acespec_verify_tail.restype = C.c_int
-    lib.acespec_verify_tail_noalloc.argtypes = [C.POINTER(ModelDesc), C.c_void_p, C.c_void_p,
+    lib.acespec_verify_tail_noalloc.argtypes = [C.POINTER(ModelDesc), C.c_void_p, C.c_int,
                                                 C.c_void_p, C.c_void_p, C.c_void_p,
-                                                C.c_void_p, C.c_int, C.c_int,
+                                                C.c_void_p, C.c_void_p, C.c_int, C.c_int,
                                                 C.POINTER(Params), C.POINTER(Outputs),
                                                 C.c_void_p]
     lib.acespec_verify_tail_noalloc.restype = C.c_int
@@ -161,21 +162,21 @@ def acespec_verify_tree_scalar_q(ctx, weights: Weights, kv: KVCache, tree_tokens
                                                       stream))
 
 
-def acespec_verify_tail(ctx, lm_head: int, final_norm: Optional[int], hidden: int,
-                        draft_tokens: int, draft_q: int, uniforms: int, R: int, chain_len: int,
-                        params: Params, outputs: Outputs, stream: int) -> int:
-    return _check(load().acespec_verify_tail(ctx, lm_head, final_norm, hidden, draft_tokens,
-                                             draft_q, uniforms, R, chain_len, C.byref(params),
-                                             C.byref(outputs), stream))
+def acespec_verify_tail(ctx, lm_head: int, lm_head_layout: int, final_norm: Optional[int],
+                        hidden: int, draft_tokens: int, draft_q: int, uniforms: int, R: int,
+                        chain_len: int, params: Params, outputs: Outputs, stream: int) -> int:
+    return _check(load().acespec_verify_tail(ctx, lm_head, lm_head_layout, final_norm, hidden,
+                                             draft_tokens, draft_q, uniforms, R, chain_len,
+                                             C.byref(params), C.byref(outputs), stream))
 
 
-def acespec_verify_tail_noalloc(desc: ModelDesc, lm_head: int, final_norm: Optional[int],
-                                hidden: int, draft_tokens: int, draft_q: int, uniforms: int,
-                                R: int, chain_len: int, params: Params, outputs: Outputs,
-                                stream: int) -> int:
-    return _check(load().acespec_verify_tail_noalloc(C.byref(desc), lm_head, final_norm, hidden,
-                                                     draft_tokens, draft_q, uniforms, R,
-                                                     chain_len, C.byref(params),
+def acespec_verify_tail_noalloc(desc: ModelDesc, lm_head: int, lm_head_layout: int,
+                                final_norm: Optional[int], hidden: int, draft_tokens: int,
+                                draft_q: int, uniforms: int, R: int, chain_len: int,
+                                params: Params, outputs: Outputs, stream: int) -> int:
+    return _check(load().acespec_verify_tail_noalloc(C.byref(desc), lm_head, lm_head_layout,
+                                                     final_norm, hidden, draft_tokens, draft_q,
+                                                     uniforms, R, chain_len, C.byref(params),
                                                      C.byref(outputs), stream))
 
 
@@ -339,9 +340,11 @@ class Verifier:
                                  n1 - 1, _ptr(new_prefix_len), self._stream())
 
     def verify_tail(self, lm_head, final_norm, hidden, draft, q, u, chain_len: int, T: float,
-                    top_p: float, k: int, outs: Dict) -> int:
+                    top_p: float, k: int, outs: Dict, packed: bool = False) -> int:
+        """packed: lm_head is the flat output of pack_weights (acespec_pack_weight)."""
         R = hidden.shape[0]
-        return acespec_verify_tail(self.ctx, _ptr(lm_head), _ptr(final_norm), _ptr(hidden),
-                                   _ptr(draft), _ptr(q), _ptr(u), R, chain_len,
-                                   Params(T, top_p, k), self.outputs_struct(outs),
-                                   self._stream())
+        return acespec_verify_tail(self.ctx, _ptr(lm_head),
+                                   ACESPEC_LAYOUT_PACKED if packed else ACESPEC_LAYOUT_ROWS,
+                                   _ptr(final_norm), _ptr(hidden), _ptr(draft), _ptr(q),
+                                   _ptr(u), R, chain_len, Params(T, top_p, k),
+                                   self.outputs_struct(outs), self._stream())

@@ -117,6 +117,17 @@ int run(acespec_ctx *c, int kind, hipStream_t s, F &&launch) {
     if (rc_ != ACESPEC_OK) return rc_;                               \
   } while (0)
 
+// The storage of the dense matrices (acespec_layout): packed needs a bf16 model and a
+// vocabulary that is a multiple of 16.
+int check_layout(int layout, const acespec_model_desc &d) {
+  if (layout != ACESPEC_LAYOUT_ROWS && layout != ACESPEC_LAYOUT_PACKED)
+    return fail(ACESPEC_EINVAL, "unknown weight layout %d", layout);
+  if (layout == ACESPEC_LAYOUT_PACKED && (d.dtype != ACESPEC_BF16 || d.vocab % 16 != 0))
+    return fail(ACESPEC_EUNSUPPORTED,
+                "packed weights need a bf16 model with a vocabulary that is a multiple of 16");
+  return ACESPEC_OK;
+}
+
 int check_params(const acespec_params *p, int V) {
   if (!p) return fail(ACESPEC_EINVAL, "params is NULL");
   if (!(p->temperature > 0.f) || !std::isfinite(p->temperature))
@@ -291,12 +302,12 @@ int verify_tail_run(acespec_ctx *ctx, const acespec_model_desc &d, const TailWor
 }
 
 template <typename T>
-int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
+int verify_tail_impl(acespec_ctx *ctx, const void *lm_head, int packed, const void *final_norm,
                      const void *hidden, const int32_t *draft, const float *draft_q,
                      const float *uniforms, int R, int chain_len, const acespec_params *p,
                      const acespec_outputs *o, hipStream_t stream) {
   const TailWorkspace ws{ctx->logits, ctx->tile_max, ctx->cand, kCandCap, ctx->rowflag, ctx->a,
-                         GemmAux{ctx->gpart, ctx->gpart_cap, ctx->cus}};
+                         GemmAux{ctx->gpart, ctx->gpart_cap, ctx->cus, packed}};
   return verify_tail_run<T>(ctx, ctx->d, ws, lm_head, final_norm, hidden, draft, draft_q,
                             uniforms, R, chain_len, p, o, stream);
 }
@@ -454,11 +465,10 @@ int verify_tree_checked(acespec_ctx *ctx, const acespec_weights *w, const acespe
     if (!lw.attn_norm || !lw.wqkv || !lw.wo || !lw.mlp_norm || !lw.w_gate_up || !lw.w_down)
       return fail(ACESPEC_EINVAL, "layer %d has a NULL weight pointer", l);
   }
-  if (w->layout != ACESPEC_LAYOUT_ROWS && w->layout != ACESPEC_LAYOUT_PACKED)
-    return fail(ACESPEC_EINVAL, "unknown weight layout %d", (int)w->layout);
-  if (w->layout == ACESPEC_LAYOUT_PACKED && (d.dtype != ACESPEC_BF16 || d.vocab % 16 != 0))
-    return fail(ACESPEC_EUNSUPPORTED,
-                "packed weights need a bf16 model with a vocabulary that is a multiple of 16");
+  {
+    const int rc = check_layout(w->layout, d);
+    if (rc) return rc;
+  }
   if (!kv->k || !kv->v || !kv->prefix_len) return fail(ACESPEC_EINVAL, "kv cache pointer NULL");
   if (B < 1 || B > ctx->max_batch)
     return fail(ACESPEC_EINVAL, "B must be in [1, %d] (got %d)", ctx->max_batch, B);
@@ -524,28 +534,31 @@ int acespec_pack_weight(const void *src, void *dst, int rows, int cols, hipStrea
   return ACESPEC_OK;
 }
 
-int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, const void *final_norm,
-                        const void *hidden, const int32_t *draft_tokens, const float *draft_q,
-                        const float *uniforms, int R, int chain_len,
+int acespec_verify_tail(acespec_ctx *ctx, const void *lm_head, acespec_layout lm_head_layout,
+                        const void *final_norm, const void *hidden, const int32_t *draft_tokens,
+                        const float *draft_q, const float *uniforms, int R, int chain_len,
                         const acespec_params *p, const acespec_outputs *o,
                         hipStream_t stream) {
   g_err.clear();
   if (!ctx) return fail(ACESPEC_EINVAL, "ctx is NULL");
   if (!lm_head || !hidden || !draft_tokens || !draft_q || !uniforms)
     return fail(ACESPEC_EINVAL, "a required pointer is NULL");
+  int rc = check_layout(lm_head_layout, ctx->d);
+  if (rc) return rc;
+  const int packed = lm_head_layout == ACESPEC_LAYOUT_PACKED ? 1 : 0;
   if (R < 1 || R > ctx->max_rows)
     return fail(ACESPEC_EINVAL, "R must be in [1, %d] (got %d)", ctx->max_rows, R);
   if (chain_len < 1 || R % chain_len)
     return fail(ACESPEC_EINVAL, "chain_len must be >= 1 and divide R");
-  int rc = check_params(p, ctx->d.vocab);
+  rc = check_params(p, ctx->d.vocab);
   if (rc) return rc;
   rc = check_outputs(o);
   if (rc) return rc;
   if (ctx->d.dtype == ACESPEC_BF16)
-    return verify_tail_impl<bf16>(ctx, lm_head, final_norm, hidden, draft_tokens, draft_q,
-                                  uniforms, R, chain_len, p, o, stream);
-  return verify_tail_impl<float>(ctx, lm_head, final_norm, hidden, draft_tokens, draft_q,
-                                 uniforms, R, chain_len, p, o, stream);
+    return verify_tail_impl<bf16>(ctx, lm_head, packed, final_norm, hidden, draft_tokens,
+                                  draft_q, uniforms, R, chain_len, p, o, stream);
+  return verify_tail_impl<float>(ctx, lm_head, packed, final_norm, hidden, draft_tokens,
+                                 draft_q, uniforms, R, chain_len, p, o, stream);
 }
 
 int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_t *path,
@@ -684,7 +697,8 @@ int scratch_of_current_device(char **ptr, int *cus) {
 extern "C" {
 
 int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_head,
-                                const void *final_norm, const void *hidden,
+                                acespec_layout lm_head_layout, const void *final_norm,
+                                const void *hidden,
                                 const int32_t *draft_tokens, const float *draft_q,
                                 const float *uniforms, int R, int chain_len,
                                 const acespec_params *p, const acespec_outputs *o,
@@ -699,10 +713,12 @@ int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_h
                 "need d_model a multiple of 64, vocab a multiple of 4 and <= 262144");
   if (!lm_head || !hidden || !draft_tokens || !draft_q || !uniforms)
     return fail(ACESPEC_EINVAL, "a required pointer is NULL");
+  int rc = check_layout(lm_head_layout, d);
+  if (rc) return rc;
   if (R < 1) return fail(ACESPEC_EINVAL, "R must be >= 1 (got %d)", R);
   if (chain_len < 1 || R % chain_len)
     return fail(ACESPEC_EINVAL, "chain_len must be >= 1 and divide R");
-  int rc = check_params(p, d.vocab);
+  rc = check_params(p, d.vocab);
   if (rc) return rc;
   rc = check_outputs(o);
   if (rc) return rc;
@@ -734,7 +750,7 @@ int acespec_verify_tail_noalloc(const acespec_model_desc *desc, const void *lm_h
                    cand ? kCandCap : 0,
                    (int32_t *)base,
                    need_a ? (void *)(base + b_flag + b_tmax) : nullptr,
-                   GemmAux{nullptr, 0, cus}};
+                   GemmAux{nullptr, 0, cus, lm_head_layout == ACESPEC_LAYOUT_PACKED ? 1 : 0}};
   if (d.dtype == ACESPEC_BF16)
     return verify_tail_run<bf16>(nullptr, d, ws, lm_head, final_norm, hidden, draft_tokens,
                                  draft_q, uniforms, R, chain_len, p, o, stream);

@@ -90,3 +90,25 @@ def test_header_declares_the_weight_layouts():
     enum = dict((k, int(v)) for k, v in re.findall(r"\b(ACESPEC_LAYOUT_[A-Z]+)\s*=\s*(\d+)", src))
     assert enum == {"ACESPEC_LAYOUT_ROWS": A.ACESPEC_LAYOUT_ROWS,
                     "ACESPEC_LAYOUT_PACKED": A.ACESPEC_LAYOUT_PACKED}
+
+
+def test_noalloc_tail_checks_the_lm_head_layout_before_launching():
+    """acespec_verify_tail_noalloc validates lm_head_layout before touching a device (the
+    pointers below are never dereferenced): an unknown value is ACESPEC_EINVAL, a packed
+    head of an fp32 model or of a vocabulary that is not a multiple of 16 is
+    ACESPEC_EUNSUPPORTED."""
+    lib = A.load()
+    p = 0x7F0000100000
+    params = A.Params(0.8, 0.9, 8)
+    outs = A.Outputs(*([p] * 12))
+
+    def call(dtype, vocab, layout):
+        desc = A.ModelDesc(0, 256, 0, 1, 0, 0, vocab, 10000.0, 1e-5, dtype)
+        return lib.acespec_verify_tail_noalloc(A.C.byref(desc), p, layout, None, p, p, p, p,
+                                               16, 16, A.C.byref(params), A.C.byref(outs), None)
+
+    assert call(A.ACESPEC_BF16, 5008, 7) == A.ACESPEC_EINVAL
+    assert "layout" in A.acespec_last_error()
+    assert call(A.ACESPEC_F32, 5008, A.ACESPEC_LAYOUT_PACKED) == A.ACESPEC_EUNSUPPORTED
+    assert call(A.ACESPEC_BF16, 5004, A.ACESPEC_LAYOUT_PACKED) == A.ACESPEC_EUNSUPPORTED
+    assert "multiple of 16" in A.acespec_last_error()

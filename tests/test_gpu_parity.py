@@ -182,10 +182,12 @@ def test_tree_70b_widths_64_node_tree():
 # ---------------------------------------------------------------------------------------
 
 
-def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False, seed=None):
+def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False, seed=None,
+              packed=False):
     """LM-head tail through the C ABI: logits of rows_check (default all) against the
     oracle's float64 LM head; decisions of EVERY row against the oracle's verify stage on
-    the GPU's logits; the chain walk from the GPU's accept bits."""
+    the GPU's logits; the chain walk from the GPU's accept bits.  packed: the LM head in
+    the packed layout (acespec_pack_weight), the oracle on the row-major matrix."""
     from paper_2609_02514_amd.acespec import Verifier
     dev = "cuda"
     seed = w.seed_base if seed is None else seed
@@ -195,10 +197,13 @@ def _run_tail(w, W=None, rows_check=None, tol=1e-4, final_norm=False, seed=None)
     q_h, u_h, d_h = hz.host(batch.q), hz.host(batch.u), hz.host(batch.draft_tokens)
     v = Verifier.for_workload(w)
     outs = v.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, dev, True)
-    hz.log(f"verify_tail R={R} V={w.V} seed={seed}")
-    v.verify_tail(W.lm_head, W.final_norm if final_norm else None, batch.hidden,
-                  batch.draft_tokens, batch.q, batch.u, w.chain_len, w.T, w.top_p, w.top_k, outs)
+    hz.log(f"verify_tail R={R} V={w.V} seed={seed} packed={packed}")
+    lm = v.pack_weights(W).lm_head if packed else W.lm_head
+    v.verify_tail(lm, W.final_norm if final_norm else None, batch.hidden,
+                  batch.draft_tokens, batch.q, batch.u, w.chain_len, w.T, w.top_p, w.top_k, outs,
+                  packed=packed)
     torch.cuda.synchronize()
+    del lm
     g = {k: (hz.host(t) if t is not None else None) for k, t in outs.items()}
     v.close()
     rows = list(range(R)) if rows_check is None else rows_check
@@ -229,6 +234,17 @@ def test_tail_small():
     _run_tail(w)
 
 
+def test_tail_small_packed_lm_head():
+    """The LM head in the packed layout (a vocabulary that is a multiple of 16), with a
+    final norm: the same decisions as row-major against the oracle."""
+    w = synth.get("8b-lmhead-tail").scaled(name="tail-packed", d=256, V=5008, rows=96,
+                                          chain_len=8, top_k=16)
+    W = synth.make_weights(w, "cuda")
+    gain = 1.0 + synth.normal((w.d,), 0.1, torch.float32, "cuda", w.seed_base, 0, 2)
+    W = dataclasses.replace(W, final_norm=gain.to(torch.bfloat16))
+    _run_tail(w, W=W, tol=2e-3, final_norm=True, packed=True)
+
+
 def test_tail_with_final_norm():
     """A non-NULL final_norm: the tail rows are RMS-normalised with the gain (rounded to
     fp16 for the LM head) before the product; the oracle normalises in float64."""
@@ -250,14 +266,16 @@ def test_tail_fp32_model_with_final_norm():
     _run_tail(w, W=W, tol=1e-4, final_norm=True)
 
 
-def test_tail_exact_logit_ties():
-    """Duplicated LM-head rows give exactly equal logits: ties must be broken by token id
-    in the nucleus, the top-k payload and the inverse CDFs."""
+@pytest.mark.parametrize("packed", [False, True])
+def test_tail_exact_logit_ties(packed):
+    """Duplicated LM-head rows give exactly equal logits (in either layout: every output
+    column sums its products in the same order): ties must be broken by token id in the
+    nucleus, the top-k payload and the inverse CDFs."""
     w = synth.get("8b-lmhead-tail").scaled(name="tail-ties", d=128, V=4096, rows=64,
                                           chain_len=4, top_k=32, T=1.0, top_p=0.5)
     W = synth.make_weights(w, "cuda")
     W.lm_head = W.lm_head[torch.arange(w.V, device="cuda") // 8].contiguous()
-    _run_tail(w, W=W)
+    _run_tail(w, W=W, packed=packed)
 
 
 @pytest.mark.parametrize("T,top_p,top_k", [
@@ -278,11 +296,13 @@ def test_tail_parameter_extremes(T, top_p, top_k):
 @pytest.mark.parametrize("seed", hz.parity_seeds(synth.get("8b-lmhead-tail"), 3))
 def test_tail_8b_full_size(seed):
     """The LM-head tail at full size (4096 rows, vocab 128256): decisions on all rows,
-    the float64 LM head on 512 sampled rows."""
+    the float64 LM head on 512 sampled rows; even seeds with the packed LM head (the
+    benchmark's layout), odd ones row-major."""
     w = synth.get("8b-lmhead-tail")
     rng = np.random.default_rng(seed)
     rows = sorted(rng.choice(w.rows, 512, replace=False).tolist())
-    g = _run_tail(w, rows_check=rows, tol=1e-4, seed=seed)
+    packed = (seed - w.seed_base) // 100 % 2 == 0
+    g = _run_tail(w, rows_check=rows, tol=1e-4, seed=seed, packed=packed)
     rate = float(g["accept"].float().mean())
     hz.log(f"tail acceptance rate {rate:.3f}")
     assert 0.3 < rate < 0.95

@@ -20,14 +20,16 @@ def _outs(R, w):
     return A.Verifier.alloc_outputs(R, R // w.chain_len, w.chain_len, w.top_k, w.V, "cuda", True)
 
 
-@pytest.mark.parametrize("final_norm", [False, True])
-def test_noalloc_tail_equals_context_tail(final_norm):
+@pytest.mark.parametrize("final_norm,packed", [(False, False), (True, False), (False, True)])
+def test_noalloc_tail_equals_context_tail(final_norm, packed):
     w = synth.get("8b-lmhead-tail").scaled(name="tail-noalloc", rows=2048, chain_len=16)
     W = synth.make_weights(w, "cuda")
     batch = synth.make_batch(w, "cuda", weights=W)
     gain = (1.0 + synth.normal((w.d,), 0.1, torch.float32, "cuda", w.seed_base, 0, 2)).to(
         torch.bfloat16) if final_norm else None
     v = A.Verifier.for_workload(w)
+    lm = v.pack_weights(W).lm_head if packed else W.lm_head
+    layout = A.ACESPEC_LAYOUT_PACKED if packed else A.ACESPEC_LAYOUT_ROWS
     stream = torch.cuda.current_stream().cuda_stream
     # scratch layout of the entry point: row flags, LM-head maxima per 128-column tile and
     # the widened hidden states, then 4096 candidate keys a row if they still fit
@@ -38,13 +40,13 @@ def test_noalloc_tail_equals_context_tail(final_norm):
     assert not cand_fits(2048) and cand_fits(256)
     for R in (2048, 256):                 # second call: fewer rows
         ref = _outs(R, w)
-        v.verify_tail(W.lm_head, gain, batch.hidden[:R], batch.draft_tokens[:R], batch.q[:R],
-                      batch.u[:R], w.chain_len, w.T, w.top_p, w.top_k, ref)
+        v.verify_tail(lm, gain, batch.hidden[:R], batch.draft_tokens[:R], batch.q[:R],
+                      batch.u[:R], w.chain_len, w.T, w.top_p, w.top_k, ref, packed=packed)
         got = _outs(R, w)
         for t in got.values():
             if t is not None:
                 t.fill_(-7)
-        A.acespec_verify_tail_noalloc(v.desc, W.lm_head.data_ptr(),
+        A.acespec_verify_tail_noalloc(v.desc, lm.data_ptr(), layout,
                                       gain.data_ptr() if gain is not None else None,
                                       batch.hidden[:R].data_ptr(),
                                       batch.draft_tokens[:R].data_ptr(), batch.q[:R].data_ptr(),
@@ -56,7 +58,8 @@ def test_noalloc_tail_equals_context_tail(final_norm):
             if t is not None:
                 assert torch.equal(t, got[k]), (R, k)
         assert got["status"].tolist() == [0] * (R // w.chain_len)
-        hz.log(f"no-alloc tail R={R} final_norm={final_norm}: every output equals verify_tail")
+        hz.log(f"no-alloc tail R={R} final_norm={final_norm} packed={packed}: every output "
+               f"equals verify_tail")
     v.close()
 
 
@@ -66,7 +69,8 @@ def test_noalloc_rejects_rows_beyond_its_scratch():
     R = 8192
     fake = A.Outputs(*([0x1000] * 12))
     with pytest.raises(A.AcespecError) as e:
-        A.acespec_verify_tail_noalloc(desc, 0x1000, None, 0x1000, 0x1000, 0x1000, 0x1000, R, 16,
+        A.acespec_verify_tail_noalloc(desc, 0x1000, A.ACESPEC_LAYOUT_ROWS, None, 0x1000, 0x1000,
+                                      0x1000, 0x1000, R, 16,
                                       A.Params(0.6, 0.8, 8), fake,
                                       torch.cuda.current_stream().cuda_stream)
     assert e.value.code == A.ACESPEC_EINVAL and "scratch" in str(e.value)
