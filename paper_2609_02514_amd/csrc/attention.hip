@@ -12,9 +12,11 @@
 // tiles per wave, a last round of at most NW/4 tiles is split into quarter units (one
 // 16-key block of every chunk each) on the waves that would otherwise idle, merged at the
 // end through LDS.  The key range of the split streams through LDS in chunks of 64 slots:
-//  * HBM -> LDS by direct DMA (global_load_lds, 16 bytes a lane, nontemporal: the cache is
-//    read once per step, and streaming it past L2 and the MALL measured 15 % faster at
-//    the 8B shape) into a ring of NST stages.  A stage holds the chunk's keys as [64 slots][head_dim] and its values,
+//  * HBM -> LDS by direct DMA (buffer loads to LDS, 16 bytes a lane, nontemporal: the
+//    cache is read once per step, and streaming it past L2 and the MALL measured 15 %
+//    faster at the 8B shape) into a ring of NST stages.  The buffer form rather than the
+//    global one: the compiler counts it on vmcnt alone, so its waits for the fragment
+//    reads stay exact (1-3 % faster).  A stage holds the chunk's keys as [64 slots][head_dim] and its values,
 //    read from the head-dim-major value cache, as [head_dim][64 slots].  The 16-byte
 //    pieces of every row are XOR-swizzled so that the fragment reads below hit distinct
 //    banks; the DMA fixes where each lane's bytes land, so the swizzle is applied to the
@@ -118,7 +120,8 @@ AS_DEVICE int v_off(int row, int piece) { return row * KC + ((piece ^ vsw(row)) 
 // DMA of one chunk (keys key0 .. key0 + 63) into a stage: HD/8 blocks of 1 KB for K and
 // as many for V^T, dealt to the NW waves in turn.
 template <int HD, int NW, bool T32 = false>
-AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int key0,
+AS_DEVICE void issue_chunk(uint16_t *stage, __amdgpu_buffer_rsrc_t kr,
+                           __amdgpu_buffer_rsrc_t vr, int key0,
                            int capacity, int wave, int lane) {
   constexpr int BLOCKS = HD / 8;
   static_assert((2 * BLOCKS) % NW == 0, "DMA blocks per wave");
@@ -128,13 +131,13 @@ AS_DEVICE void issue_chunk(uint16_t *stage, const bf16 *kb, const bf16 *vb, int 
     if (blk < BLOCKS) {
       const int e = blk * 512 + lane * 8;          // element offset this lane's bytes land at
       const int key = e / HD, piece = (e % HD) >> 3;
-      dma16_stream(kb + (size_t)(key0 + key) * HD + ((piece ^ kswz<HD, T32>(key)) << 3),
-                   (lds_ptr_t)(stage + blk * 512));
+      buf_dma16_stream(kr, (lds_ptr_t)(stage + blk * 512),
+                       (uint32_t)((key0 + key) * HD + ((piece ^ kswz<HD, T32>(key)) << 3)) * 2u);
     } else {
       const int i = blk - BLOCKS;
       const int row = i * 8 + (lane >> 3), piece = lane & 7;
-      dma16_stream(vb + (size_t)row * capacity + key0 + ((piece ^ vsw(row)) << 3),
-                   (lds_ptr_t)(stage + KC * HD + i * 512));
+      buf_dma16_stream(vr, (lds_ptr_t)(stage + KC * HD + i * 512),
+                       (uint32_t)(row * capacity + key0 + ((piece ^ vsw(row)) << 3)) * 2u);
     }
   }
 }
@@ -198,6 +201,8 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   const int c1 = min(nchunks, c0 + cps);
   const bf16 *kb = ck + ((size_t)b * Hkv + g) * capacity * HD;
   const bf16 *vb = cv + ((size_t)b * Hkv + g) * HD * capacity;
+  const __amdgpu_buffer_rsrc_t kr = make_rsrc(kb, (uint32_t)((size_t)capacity * HD * 2));
+  const __amdgpu_buffer_rsrc_t vr = make_rsrc(vb, (uint32_t)((size_t)capacity * HD * 2));
   const size_t row0 = (size_t)b * n1;
   const int q_stride = H * HD;
   const float sscale = LOG2E / sqrtf((float)HD);   // scores -> base-2 exponent
@@ -242,7 +247,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
   // Prologue: chunks c0 .. c0+NST-2 in flight, chunk c0 widened.
 #pragma unroll
   for (int i = 0; i < NST - 1; ++i)
-    if (c0 + i < c1) issue_chunk<HD, NW>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
+    if (c0 + i < c1) issue_chunk<HD, NW>(stage_of(c0 + i), kr, vr, (c0 + i) * KC, capacity, wave, lane);
   if (c0 < c1) {
     if (c0 + NST - 2 < c1) wait_vmcnt<(NST - 2) * L_DMA>(); else wait_vmcnt<0>();
     lds_barrier();
@@ -268,7 +273,7 @@ __global__ __launch_bounds__(NW * 64) void tree_attn_mfma_kernel(
     }
     chunk_barrier();
     if (c + NST - 1 < c1)
-      issue_chunk<HD, NW>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity, wave, lane);
+      issue_chunk<HD, NW>(stage_of(c + NST - 1), kr, vr, (c + NST - 1) * KC, capacity, wave, lane);
     if (c + 1 < c1 && widener) widen_chunk<HD>(stage_of(c + 1), wt, wstride, (c + 1) * KC, total);
 
     const uint16_t *st = stage_of(c);
@@ -567,6 +572,8 @@ __global__ __launch_bounds__(512) void tree_attn_t32_kernel(
   const int c1 = min(nchunks, c0 + cps);
   const bf16 *kb = ck + ((size_t)b * Hkv + g) * capacity * HD;
   const bf16 *vb = cv + ((size_t)b * Hkv + g) * HD * capacity;
+  const __amdgpu_buffer_rsrc_t kr = make_rsrc(kb, (uint32_t)((size_t)capacity * HD * 2));
+  const __amdgpu_buffer_rsrc_t vr = make_rsrc(vb, (uint32_t)((size_t)capacity * HD * 2));
   const size_t row0 = (size_t)b * n1;
   const int q_stride = H * HD;
   const float sscale = LOG2E / sqrtf((float)HD);
@@ -624,7 +631,7 @@ __global__ __launch_bounds__(512) void tree_attn_t32_kernel(
 #pragma unroll
   for (int i = 0; i < NST - 1; ++i)
     if (c0 + i < c1)
-      issue_chunk<HD, NW, true>(stage_of(c0 + i), kb, vb, (c0 + i) * KC, capacity, wave, lane);
+      issue_chunk<HD, NW, true>(stage_of(c0 + i), kr, vr, (c0 + i) * KC, capacity, wave, lane);
   if (c0 < c1) {
     if (c0 + NST - 2 < c1) wait_vmcnt<(NST - 2) * L_DMA>(); else wait_vmcnt<0>();
     lds_barrier();
@@ -654,7 +661,7 @@ __global__ __launch_bounds__(512) void tree_attn_t32_kernel(
     }
     chunk_barrier();
     if (c + NST - 1 < c1)
-      issue_chunk<HD, NW, true>(stage_of(c + NST - 1), kb, vb, (c + NST - 1) * KC, capacity,
+      issue_chunk<HD, NW, true>(stage_of(c + NST - 1), kr, vr, (c + NST - 1) * KC, capacity,
                                 wave, lane);
     if (c + 1 < c1) widen_chunk<HD>(stage_of(c + 1), wt, wstride, (c + 1) * KC, total);
 

@@ -90,17 +90,6 @@ AS_DEVICE int wave_sum_i32(int v) {
 // ------------------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
-// One wave copies 64 x 16 bytes: lane i reads its own global address g and the bytes land
-// at l + 16 i (l is wave-uniform).  Completion is counted by vmcnt like any load.
-AS_DEVICE void dma16(const void *g, lds_ptr_t l) {
-  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
-}
-// The same with the nontemporal cache policy, for data read once per step (the KV cache
-// streamed by attention): measured on MI355X, streaming reads with it run at about
-// 6.4 TB/s against 5.0-5.4 TB/s without (they do not allocate in L2 or the MALL).
-AS_DEVICE void dma16_stream(const void *g, lds_ptr_t l) {
-  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 2 /* nt */);
-}
 // A 16-byte global load with the nontemporal cache policy (last read of a stream).
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 AS_DEVICE float4 ld_stream(const float *p) {
@@ -108,10 +97,20 @@ AS_DEVICE float4 ld_stream(const float *p) {
   return make_float4(t.x, t.y, t.z, t.w);
 }
 
-// The same through a buffer resource: lane i reads rsrc + voff + soff (soff scalar, so a
-// moving k offset costs no vector arithmetic); reads past the resource's size return 0.
+// One wave copies 64 x 16 bytes through a buffer resource: lane i reads rsrc + voff + soff
+// (soff scalar, so a moving k offset costs no vector arithmetic) and the bytes land at
+// l + 16 i (l is wave-uniform); reads past the resource's size return 0.  Completion is
+// counted by vmcnt like any load.
 AS_DEVICE void buf_dma16(__amdgpu_buffer_rsrc_t rsrc, lds_ptr_t l, uint32_t voff, int soff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, l, 16, voff, soff, 0, 0);
+}
+// The same with the nontemporal cache policy, for data read once per step (the KV cache):
+// measured on MI355X, streaming reads with it run at about 6.4 TB/s against 5.0-5.4 TB/s
+// without (they do not allocate in L2 or the MALL).  Unlike the global-address form of the
+// LDS DMA, the compiler counts this one on vmcnt alone, so its waits for LDS reads issued
+// after it stay exact instead of waiting for every outstanding LDS access.
+AS_DEVICE void buf_dma16_stream(__amdgpu_buffer_rsrc_t rsrc, lds_ptr_t l, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, l, 16, voff, 0, 0, 2 /* nt */);
 }
 AS_DEVICE __amdgpu_buffer_rsrc_t make_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
