@@ -380,6 +380,7 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
     const int hd = ro.hd, half = hd >> 1, nheads = ro.H + 2 * ro.Hkv;
     const int lq4 = hd == 128 ? 4 : 3;  // log2 of the 4-frequency items per row (hd 64 or 128)
     for (int c0 = 0; c0 < TBM; c0 += CR) {
+      const int nr = TBM - c0 < CR ? TBM - c0 : CR;  // rows of this part (tiles of 112 rows)
       __syncthreads();  // every wave is past the ring / the previous part
       if (tid < CR) {
         const int row = m0 + c0 + tid;
@@ -404,7 +405,7 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
         if (gh >= nheads) break;
         const float *sb = st + hb * hd;
         if (gh < ro.H + ro.Hkv) {  // query or key head: rotate-half, 4 frequencies a thread
-          for (int it = tid; it < (CR << lq4); it += NW * 64) {
+          for (int it = tid; it < (nr << lq4); it += NW * 64) {
             const int r = it >> lq4, i = (it & ((1 << lq4) - 1)) * 4, row = m0 + c0 + r;
             if (row >= M) continue;
             const float4 a1 = *(const float4 *)(sb + r * SP + i);
@@ -438,7 +439,7 @@ __global__ __launch_bounds__(WMN * WNN * (PK == 2 ? 2 : 1) * 64, OCC) void gemm_
           const int g = gh - ro.H - ro.Hkv;
           for (int it = tid; it < CR * hd; it += NW * 64) {
             const int dd = it / CR, r = it - dd * CR, row = m0 + c0 + r;
-            if (row >= M) continue;
+            if (r >= nr || row >= M) continue;
             ro.cv[(((size_t)rsess[r] * ro.Hkv + g) * hd + dd) * ro.capacity + rslot[r]] =
                 from_f32<TB>(sb[r * SP + dd]);
           }
@@ -757,6 +758,7 @@ constexpr GemmVariant kVariants[] = {
     {2, 2, 4, 4, 4, 1, 64, 2},  // 10: 128 x 128, two groups of 4 waves of 64 x 64 splitting k
     {1, 8, 8, 4, 4, 1, 32, 1},  // 11: 128 x 512, 8 waves of 128 x 64, 32 KB ring, 1 WG per CU
     {1, 8, 4, 4, 4, 1, 32, 1},  // 12: 64 x 512, 8 waves of 64 x 64, 16 KB ring, 1 WG per CU
+    {1, 4, 7, 4, 4, 1, 64, 2},  // 13: 112 x 256, two groups of 4 waves of 112 x 64 splitting k
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
@@ -830,7 +832,7 @@ void launch_epi(int var, hipStream_t s, const f16 *A, const TB *W, int M, int N,
     if constexpr (kVariants[V].pk != 2 || EPI == acespec::EPI_QKV_ROPE)                     \
       launch_variant<EPI, V, TB>(s, A, W, M, N, K, out, outf, part, mt, nt, sp, ro, tmax);  \
     break;
-    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9) CASE(10) CASE(11) CASE(12)
+    CASE(0) CASE(1) CASE(2) CASE(3) CASE(4) CASE(5) CASE(6) CASE(7) CASE(8) CASE(9) CASE(10) CASE(11) CASE(12) CASE(13)
 #undef CASE
     default: break;
   }
@@ -1006,9 +1008,10 @@ hipError_t launch_qkv_rope<bf16, f16>(const f16 *A, const bf16 *W, int M, int N,
   const bool fusable = N == (ro.H + 2 * ro.Hkv) * ro.hd;
   if (aux.packed && M > 384 && fusable && 128 % ro.hd == 0) {
     // tiles kept whole, each with two wave groups splitting its k-steps (two waves a SIMD
-    // with about one tile a CU), RoPE and cache write in the epilogue: 128 x 256 tiles from
-    // ~1k rows, 128 x 128 below
-    const int gv = M >= 1024 ? 9 : 10;
+    // with about one tile a CU), RoPE and cache write in the epilogue: 112 x 256 tiles from
+    // ~1k rows (1088 rows: 240 tiles for 256 CUs and 32 padding rows, against 216 tiles and
+    // 64 rows at 128 x 256), 128 x 128 below
+    const int gv = M >= 1024 ? 13 : 10;
     const GemmVariant g = kVariants[gv];
     const int mt = (M + g.wtm * 16 * g.wmn - 1) / (g.wtm * 16 * g.wmn);
     const int nt = (N + g.wtn * 16 * g.wnn - 1) / (g.wtn * 16 * g.wnn);
