@@ -364,6 +364,13 @@ def lds_patterns():
             out.append(2 * (key * 128 + (((s * 4 + (l >> 4)) ^ sw(key)) << 3)))
         return out
 
+    def p32(r):   # key held by A row r of the 32-row-tile kernel's 32 x 32 score block
+        return ((r >> 4) & 1) * 16 + ((r >> 2) & 1) * 8 + ((r >> 3) & 1) * 4 + (r & 3)
+
+    def attn_k32(sw, s=0):   # its key fragments: row p32(l % 32), logical piece 2 s + l / 32
+        return [2 * (p32(l & 31) * 128 + (((2 * s + (l >> 5)) ^ sw(p32(l & 31))) << 3))
+                for l in range(64)]
+
     def attn_v(sw, ks=0, nb=0):  # 128-byte V^T rows (64 slots)
         out = []
         for l in range(64):
@@ -379,6 +386,11 @@ def lds_patterns():
         ("attention K rows, key swizzle", attn_k(lambda k: (((k >> 3) & 3) << 2) | (k & 3))),
         ("attention V^T rows, row ^ (row / 8)", attn_v(lambda r: (r & 7) ^ ((r >> 3) & 1))),
         ("attention V^T rows, row / 2", attn_v(lambda r: (r >> 1) & 7)),
+        ("attention 32-row tiles, K rows, its key swizzle",
+         attn_k32(lambda k: (k & 0xB) | ((((k >> 2) ^ (k >> 4)) & 1) << 2))),
+        ("attention 32-row tiles, K rows, the 16-row kernel's key swizzle",
+         attn_k32(lambda k: (((k >> 3) & 3) << 2) | (k & 3))),
+        ("attention 32-row tiles, K rows, piece ^ (key % 16)", attn_k32(lambda k: k & 15)),
     ]
 
 
