@@ -264,6 +264,26 @@ int acespec_commit_kv(acespec_ctx *ctx, const acespec_kv_cache *kv, const int32_
  * Enqueued on stream; ACESPEC_EINVAL for a NULL pointer or a shape outside the above. */
 int acespec_pack_weight(const void *src, void *dst, int rows, int cols, hipStream_t stream);
 
+/* Value-cache layout conversion, for callers that keep values slot-major like the keys
+ * (v[planes][capacity][head_dim], slot s of a head is row s): the verify step reads the
+ * head-dim-major layout of acespec_kv_cache (v[planes][head_dim][capacity]), in which the
+ * attention's sum over slots (Section III-C) streams contiguous memory.  Not part of the
+ * verify step: a caller converts a session's prefix once when it loads it, and converts
+ * back when it needs slot-major values again.
+ *  planes     = n_layers * B * n_kv_heads (the leading dimensions, same order in both),
+ *  capacity   slots per plane, a positive multiple of 64 (as in acespec_kv_cache),
+ *  head_dim   >= 1,  dtype: ACESPEC_BF16 or ACESPEC_F32 (element size 2 or 4 bytes),
+ *  direction  ACESPEC_V_TO_HEAD_DIM_MAJOR (src slot-major) or ACESPEC_V_TO_SLOT_MAJOR
+ *             (src head-dim-major, the inverse),
+ *  src, dst   DEVICE, caller-owned, planes*capacity*head_dim elements each, no overlap.
+ * Values are copied bit for bit.  Enqueued on stream; ACESPEC_EINVAL (nothing launched)
+ * for a NULL pointer, overlap, an unknown dtype or direction, a size outside the above,
+ * or more than 2^31 - 1 tiles of 32 x 32 (convert in parts). */
+typedef enum { ACESPEC_V_TO_HEAD_DIM_MAJOR = 0, ACESPEC_V_TO_SLOT_MAJOR = 1 } acespec_v_direction;
+int acespec_convert_v_cache(const void *src, void *dst, int planes, int capacity, int head_dim,
+                            acespec_dtype dtype, acespec_v_direction direction,
+                            hipStream_t stream);
+
 /* Message for the last non-OK return on this thread ("" if none). */
 const char *acespec_last_error(void);
 

@@ -21,7 +21,8 @@ ACESPEC_F32, ACESPEC_BF16 = 0, 1
 EXPORTED = ["acespec_create", "acespec_destroy", "acespec_verify_tree",
             "acespec_verify_tree_scalar_q", "acespec_verify_tail", "acespec_commit_kv",
             "acespec_last_error", "acespec_timing_enable", "acespec_timing_read",
-            "acespec_timing_only", "acespec_verify_tail_noalloc", "acespec_pack_weight"]
+            "acespec_timing_only", "acespec_verify_tail_noalloc", "acespec_pack_weight",
+            "acespec_convert_v_cache"]
 
 
 class ModelDesc(C.Structure):
@@ -37,6 +38,7 @@ class LayerWeights(C.Structure):
 
 
 ACESPEC_LAYOUT_ROWS, ACESPEC_LAYOUT_PACKED = 0, 1
+ACESPEC_V_TO_HEAD_DIM_MAJOR, ACESPEC_V_TO_SLOT_MAJOR = 0, 1
 
 
 class Weights(C.Structure):
@@ -101,6 +103,9 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.acespec_commit_kv.restype = C.c_int
     lib.acespec_pack_weight.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_void_p]
     lib.acespec_pack_weight.restype = C.c_int
+    lib.acespec_convert_v_cache.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_int,
+                                            C.c_int, C.c_int, C.c_void_p]
+    lib.acespec_convert_v_cache.restype = C.c_int
     lib.acespec_last_error.argtypes = []
     lib.acespec_last_error.restype = C.c_char_p
     lib.acespec_timing_enable.argtypes = [C.c_void_p, C.c_int]
@@ -188,6 +193,12 @@ def acespec_commit_kv(ctx, kv: KVCache, path: int, path_len: int, status: Option
 
 def acespec_pack_weight(src: int, dst: int, rows: int, cols: int, stream: int) -> int:
     return _check(load().acespec_pack_weight(src, dst, rows, cols, stream))
+
+
+def acespec_convert_v_cache(src: int, dst: int, planes: int, capacity: int, head_dim: int,
+                            dtype: int, direction: int, stream: int) -> int:
+    return _check(load().acespec_convert_v_cache(src, dst, planes, capacity, head_dim, dtype,
+                                                 direction, stream))
 
 
 def acespec_timing_enable(ctx, enable: bool) -> None:

@@ -492,6 +492,13 @@ int verify_tree_checked(acespec_ctx *ctx, const acespec_weights *w, const acespe
 
 }  // namespace
 
+namespace acespec {
+// commit.hip: each of `planes` [rows][cols] matrices of elem_bytes-wide elements (2 or 4),
+// written transposed as [cols][rows] to dst (no overlap).
+hipError_t launch_transpose_planes(const void *src, void *dst, int elem_bytes, int planes,
+                                   int rows, int cols, hipStream_t s);
+}  // namespace acespec
+
 extern "C" {
 
 int acespec_verify_tree(acespec_ctx *ctx, const acespec_weights *w, const acespec_kv_cache *kv,
@@ -531,6 +538,33 @@ int acespec_pack_weight(const void *src, void *dst, int rows, int cols, hipStrea
   if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(ACESPEC_EINVAL, "src and dst overlap");
   const hipError_t e = launch_pack_weights((const bf16 *)src, (f16 *)dst, rows, cols, stream);
   if (e != hipSuccess) return fail(ACESPEC_EHIP, "pack launch: %s", hipGetErrorString(e));
+  return ACESPEC_OK;
+}
+
+int acespec_convert_v_cache(const void *src, void *dst, int planes, int capacity, int head_dim,
+                            acespec_dtype dtype, acespec_v_direction direction,
+                            hipStream_t stream) {
+  g_err.clear();
+  if (!src || !dst) return fail(ACESPEC_EINVAL, "src or dst is NULL");
+  if (dtype != ACESPEC_BF16 && dtype != ACESPEC_F32)
+    return fail(ACESPEC_EINVAL, "dtype must be ACESPEC_BF16 or ACESPEC_F32 (got %d)", (int)dtype);
+  if (direction != ACESPEC_V_TO_HEAD_DIM_MAJOR && direction != ACESPEC_V_TO_SLOT_MAJOR)
+    return fail(ACESPEC_EINVAL, "unknown direction %d", (int)direction);
+  if (planes < 1 || head_dim < 1 || capacity < 64 || capacity % 64 != 0)
+    return fail(ACESPEC_EINVAL,
+                "planes and head_dim must be >= 1 and capacity a positive multiple of 64 "
+                "(got %d, %d, %d)", planes, head_dim, capacity);
+  const int eb = dtype == ACESPEC_BF16 ? 2 : 4;
+  const long long tiles = (long long)planes * ((capacity + 31) / 32) * ((head_dim + 31) / 32);
+  if (tiles > 0x7fffffffLL)
+    return fail(ACESPEC_EINVAL, "%lld tiles of 32 x 32 exceed one launch: convert in parts", tiles);
+  const size_t bytes = (size_t)planes * capacity * head_dim * eb;
+  const char *s0 = (const char *)src, *d0 = (const char *)dst;
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return fail(ACESPEC_EINVAL, "src and dst overlap");
+  const bool to_hd = direction == ACESPEC_V_TO_HEAD_DIM_MAJOR;
+  const hipError_t e = acespec::launch_transpose_planes(src, dst, eb, planes, to_hd ? capacity : head_dim,
+                                               to_hd ? head_dim : capacity, stream);
+  if (e != hipSuccess) return fail(ACESPEC_EHIP, "convert launch: %s", hipGetErrorString(e));
   return ACESPEC_OK;
 }
 

@@ -63,6 +63,35 @@ __global__ __launch_bounds__(256) void commit_kv_kernel(T *__restrict__ ck, T *_
   }
 }
 
+
+// Value-cache layout conversion (not part of the verify step): every plane (layer,
+// session, kv head) is a [rows][cols] matrix, written transposed as [cols][rows] --
+// slot-major [capacity][head_dim] <-> the head-dim-major [head_dim][capacity] the verify
+// step reads.  32 x 32 tiles pass through LDS so that reads and writes both run along
+// rows; elements move as raw bits (E: 2 or 4 bytes).  One workgroup per tile.
+template <typename E>
+__global__ __launch_bounds__(256) void transpose_planes_kernel(const E *__restrict__ src,
+                                                               E *__restrict__ dst, int rows,
+                                                               int cols, int tiles_r,
+                                                               int tiles_c) {
+  __shared__ E tile[32][33];
+  const int per_plane = tiles_r * tiles_c;
+  const long long plane = blockIdx.x / per_plane;
+  const int t = (int)(blockIdx.x - plane * per_plane);
+  const int tr = t / tiles_c, tc = t - tr * tiles_c;
+  const size_t base = (size_t)plane * rows * cols;
+  const int x = threadIdx.x & 31, y = threadIdx.x >> 5;  // 32 x 8 threads
+  for (int i = y; i < 32; i += 8) {
+    const int r = tr * 32 + i, c = tc * 32 + x;
+    if (r < rows && c < cols) tile[i][x] = src[base + (size_t)r * cols + c];
+  }
+  __syncthreads();
+  for (int i = y; i < 32; i += 8) {
+    const int c = tc * 32 + i, r = tr * 32 + x;  // destination row c, column r
+    if (c < cols && r < rows) dst[base + (size_t)c * rows + r] = tile[x][i];
+  }
+}
+
 }  // namespace
 
 namespace acespec {
@@ -84,5 +113,21 @@ template hipError_t launch_commit_kv<float>(float *, float *, const int32_t *, c
 template hipError_t launch_commit_kv<bf16>(bf16 *, bf16 *, const int32_t *, const int32_t *,
                                            const int32_t *, const int32_t *, int, int, int, int,
                                            int, int, int32_t *, hipStream_t);
+
+hipError_t launch_transpose_planes(const void *src, void *dst, int elem_bytes, int planes,
+                                   int rows, int cols, hipStream_t s) {
+  if (planes < 1 || rows < 1 || cols < 1 || (elem_bytes != 2 && elem_bytes != 4))
+    return hipErrorInvalidValue;
+  const int tiles_r = (rows + 31) / 32, tiles_c = (cols + 31) / 32;
+  const long long blocks = (long long)planes * tiles_r * tiles_c;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(transpose_planes_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, s,
+                       (const uint16_t *)src, (uint16_t *)dst, rows, cols, tiles_r, tiles_c);
+  else
+    hipLaunchKernelGGL(transpose_planes_kernel<uint32_t>, dim3((unsigned)blocks), dim3(256), 0, s,
+                       (const uint32_t *)src, (uint32_t *)dst, rows, cols, tiles_r, tiles_c);
+  return hipGetLastError();
+}
 
 }  // namespace acespec

@@ -85,6 +85,39 @@ def test_pack_weight_rejects_bad_shapes_and_overlap_before_launching():
     assert "overlap" in A.acespec_last_error()
 
 
+def test_convert_v_cache_rejects_bad_arguments_before_launching():
+    """acespec_convert_v_cache checks its arguments before anything is enqueued (the
+    pointers below are never dereferenced)."""
+    lib = A.load()
+    src, dst = 0x7F0000100000, 0x7F0010000000
+    to_hd = A.ACESPEC_V_TO_HEAD_DIM_MAJOR
+
+    def conv(s=src, d=dst, planes=4, cap=128, hd=64, dt=A.ACESPEC_BF16, direction=to_hd):
+        return lib.acespec_convert_v_cache(s, d, planes, cap, hd, dt, direction, None)
+
+    assert conv(s=None) == A.ACESPEC_EINVAL and "NULL" in A.acespec_last_error()
+    assert conv(d=None) == A.ACESPEC_EINVAL
+    assert conv(dt=7) == A.ACESPEC_EINVAL and "dtype" in A.acespec_last_error()
+    assert conv(direction=2) == A.ACESPEC_EINVAL and "direction" in A.acespec_last_error()
+    for planes, cap, hd in ((0, 128, 64), (4, 100, 64), (4, 0, 64), (4, 128, 0)):
+        assert conv(planes=planes, cap=cap, hd=hd) == A.ACESPEC_EINVAL
+        assert "multiple of 64" in A.acespec_last_error()
+    # 2^30 planes of 2 x 2 tiles: more than one launch holds
+    assert conv(planes=1 << 30, cap=64, hd=64) == A.ACESPEC_EINVAL
+    assert "in parts" in A.acespec_last_error()
+    # dst starting inside src's 4 x 128 x 64 x 2 = 64 KB; fp32 doubles the extent
+    assert conv(d=src + 60000) == A.ACESPEC_EINVAL and "overlap" in A.acespec_last_error()
+    assert conv(d=src + 100000, dt=A.ACESPEC_F32) == A.ACESPEC_EINVAL
+    assert "overlap" in A.acespec_last_error()
+
+
+def test_header_declares_the_v_cache_directions():
+    src = open(os.path.join(ROOT, "include", "acespec.h")).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"\b(ACESPEC_V_TO_[A-Z_]+)\s*=\s*(\d+)", src))
+    assert enum == {"ACESPEC_V_TO_HEAD_DIM_MAJOR": A.ACESPEC_V_TO_HEAD_DIM_MAJOR,
+                    "ACESPEC_V_TO_SLOT_MAJOR": A.ACESPEC_V_TO_SLOT_MAJOR}
+
+
 def test_header_declares_the_weight_layouts():
     src = open(os.path.join(ROOT, "include", "acespec.h")).read()
     enum = dict((k, int(v)) for k, v in re.findall(r"\b(ACESPEC_LAYOUT_[A-Z]+)\s*=\s*(\d+)", src))

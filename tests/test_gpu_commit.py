@@ -111,3 +111,33 @@ def test_commit_after_verify_equals_causal_decode_cache():
             hz.log(f"layer {l}: committed cache rel err {err:.2e}")
             assert err < 2e-2
     v.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_convert_v_cache_is_an_exact_transpose_both_ways(dtype):
+    """acespec_convert_v_cache against torch's transpose, bit for bit: a slot-major value
+    cache [planes, cap, hd] becomes the head-dim-major [planes, hd, cap] the verify step
+    reads, and back.  Ragged head_dim (40: a partial 32-wide tile) and a capacity of 3 x 64
+    slots check the tile edges; NaN and inf bit patterns must survive."""
+    from paper_2609_02514_amd import acespec as A
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    adt = A.ACESPEC_BF16 if dtype == "bf16" else A.ACESPEC_F32
+    for planes, cap, hd in ((3, 192, 40), (64, 128, 128)):
+        hz.log(f"convert_v_cache {dtype} planes={planes} cap={cap} hd={hd}")
+        g = torch.Generator(device="cpu").manual_seed(planes * 1000 + cap + hd)
+        slot_major = torch.randn(planes, cap, hd, generator=g).to(tdt)
+        slot_major[0, 5, 3] = float("nan")
+        slot_major[-1, -1, -1] = float("inf")
+        slot_major = slot_major.cuda()
+        hd_major = torch.empty(planes, hd, cap, dtype=tdt, device="cuda")
+        back = torch.empty_like(slot_major)
+        stream = torch.cuda.current_stream().cuda_stream
+        A.acespec_convert_v_cache(slot_major.data_ptr(), hd_major.data_ptr(), planes, cap, hd,
+                                  adt, A.ACESPEC_V_TO_HEAD_DIM_MAJOR, stream)
+        A.acespec_convert_v_cache(hd_major.data_ptr(), back.data_ptr(), planes, cap, hd, adt,
+                                  A.ACESPEC_V_TO_SLOT_MAJOR, stream)
+        torch.cuda.synchronize()
+        iview = torch.int16 if dtype == "bf16" else torch.int32
+        want = slot_major.transpose(1, 2).contiguous()
+        assert torch.equal(hd_major.view(iview), want.view(iview))
+        assert torch.equal(back.view(iview), slot_major.view(iview))
