@@ -58,6 +58,10 @@ def test_tree_tiny_fp32_full_config(seed):
     # 8 query heads per kv head under a 64-node tree: 520 query rows, two query groups
     dict(hd=64, H=16, Hkv=2, d=256, tree="chain_sib", depth=8, sib=7, B=2, S=300, top_k=32),
     dict(hd=128, H=8, Hkv=1, d=256, tree="chain_sib", depth=8, sib=7, B=3, S=200, V=3000),
+    # 8 query heads under a 36-node tree: 296 rows in two query groups of 148, i.e. four
+    # 32-row tiles and a 20-row remainder, which is a padded 32-row tile of its own
+    dict(hd=64, H=16, Hkv=2, d=256, tree="chain_sib", depth=4, sib=8, B=2, S=1024, V=3000),
+    dict(hd=128, H=16, Hkv=2, d=256, tree="chain_sib", depth=4, sib=8, B=2, S=600, V=3000),
 ])
 def test_tree_small_bf16(variant):
     w = small_bf16(**variant)
