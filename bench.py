@@ -494,8 +494,8 @@ def main():
     w = synth.get(args.workload)
     tail = w.tree == "tail"
     log(f"generating {w.name} on the GPU")
-    W = synth.make_weights(w, "cuda")
-    batch = synth.make_batch(w, "cuda")
+    W = synth.make_weights(w, "cuda", progress=log)
+    batch = synth.make_batch(w, "cuda", progress=log)
     v = Verifier.for_workload(w)
     if args.layout == "auto":
         args.layout = "packed" if w.dtype == "bf16" else "rows"

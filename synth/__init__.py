@@ -245,7 +245,9 @@ class Weights:
                        mv(self.final_norm), mv(self.lm_head))
 
 
-def make_weights(w: Workload, device="cpu", seed: Optional[int] = None) -> Weights:
+def make_weights(w: Workload, device="cpu", seed: Optional[int] = None,
+                 progress=None) -> Weights:
+    """Random-init weights of ``w``; progress(msg), if given, hears every 8th layer."""
     seed = w.seed_base if seed is None else seed
     dt = _torch_dtype(w)
     std = 0.02
@@ -268,6 +270,8 @@ def make_weights(w: Workload, device="cpu", seed: Optional[int] = None) -> Weigh
             w_gate_up=normal((2 * w.F, w.d), std, dt, device, seed, 0, base + 4),
             w_down=normal((w.d, w.F), std, dt, device, seed, 0, base + 5),
         ))
+        if progress is not None and ((l + 1) % 8 == 0 or l + 1 == w.L):
+            progress(f"weights: {l + 1}/{w.L} layers")
     embed = normal((w.V, w.d), std, dt, device, seed, 0, 1) if w.L > 0 else None
     final_norm = gain(2) if w.L > 0 else None
     lm_head = normal((w.V, w.d), std, dt, device, seed, 0, 3)
@@ -301,7 +305,7 @@ def prefix_lengths(w: Workload, seed: int) -> List[int]:
     return [int(x) for x in torch.randint(lo, w.S + 1, (w.B,), generator=g)]
 
 
-def make_kv(w: Workload, device, seed: int, cap: int):
+def make_kv(w: Workload, device, seed: int, cap: int, progress=None):
     dt = _torch_dtype(w)
     kshape = (w.L, w.B, w.Hkv, cap, w.hd)
     vshape = (w.L, w.B, w.Hkv, w.hd, cap)
@@ -310,6 +314,8 @@ def make_kv(w: Workload, device, seed: int, cap: int):
     for l in range(w.L):   # per layer, to bound the fp32 staging memory
         k[l].copy_(normal(kshape[1:], 1.0, dt, device, seed, 1, 2 * l))
         v[l].copy_(normal(vshape[1:], 1.0, dt, device, seed, 1, 2 * l + 1))
+        if progress is not None and ((l + 1) % 8 == 0 or l + 1 == w.L):
+            progress(f"KV cache: {l + 1}/{w.L} layers")
     return k, v
 
 
@@ -319,8 +325,9 @@ def draft_q(w: Workload, rows_shape, device, seed: int) -> torch.Tensor:
 
 
 def make_batch(w: Workload, device="cpu", seed: Optional[int] = None,
-               weights: Optional[Weights] = None, extra_cap: int = 0) -> Batch:
-    """Draw one batch of drafted trees (or tail rows) for workload ``w``."""
+               weights: Optional[Weights] = None, extra_cap: int = 0, progress=None) -> Batch:
+    """Draw one batch of drafted trees (or tail rows) for workload ``w``; progress(msg), if
+    given, hears every 8th layer of the KV cache."""
     seed = w.seed_base if seed is None else seed
     if w.tree == "tail":
         return _make_tail(w, device, seed, weights)
@@ -352,7 +359,7 @@ def make_batch(w: Workload, device="cpu", seed: Optional[int] = None,
                     tok[:, c] = sib[:, j]
     S_list = prefix_lengths(w, seed)
     cap = (max(S_list) + n1 + extra_cap + 63) // 64 * 64
-    kv_k, kv_v = make_kv(w, device, seed, cap)
+    kv_k, kv_v = make_kv(w, device, seed, cap, progress)
     return Batch(tokens=tok.to(torch.int32), parents=par.to(device),
                  prefix_len=torch.tensor(S_list, dtype=torch.int32, device=device),
                  kv_k=kv_k, kv_v=kv_v, q=q, u=u, cap=cap)
